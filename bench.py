@@ -1,0 +1,196 @@
+"""Benchmark of the MicroMix hot path on one MI355X.
+
+A step is one pass of the online path over one batch: fused reorder-and-
+quantize of the bf16 activation (mm_quantize_act) followed by the mixed
+MXFP4/6/8 GEMM (mm_gemm) against an offline-quantised weight.  Weight
+quantisation (mm_quantize_weight) runs once per weight and is timed apart.
+
+Prints one JSON line: whole-step throughput in TFLOP/s (2 M N K per step),
+the GEMM's roofline against the MFMA peak of its bit mix, the quantiser's HBM
+bandwidth, and the CPU oracle timed on the host as a baseline.
+
+Inputs are seeded synthetic tensors resident in HBM before the timed region;
+several buffer sets are rotated so the working set exceeds the 256 MB
+Infinity Cache.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published dense peaks (TFLOP/s) and HBM bandwidth (GB/s).
+PEAK_FP4_FP6 = 10100.0
+PEAK_FP8 = 5000.0
+PEAK_HBM = 8000.0
+
+
+def mix_peak_tflops(split) -> float:
+    """MFMA peak for the bit mix: FP4 and FP6 run at the FP4 rate, FP8 at half."""
+    p4, p6, p8 = split
+    K = p4 + p6 + p8
+    t = (p4 + p6) / K / PEAK_FP4_FP6 + p8 / K / PEAK_FP8
+    return 1.0 / t
+
+
+def quant_bytes(rows: int, K: int, split) -> int:
+    """Algorithmic bytes of one quantiser launch: bf16 read, codes and scales
+    written, sigma read once."""
+    p4, p6, p8 = split
+    return rows * K * 2 + rows * (p4 // 2 + 3 * p6 // 4 + p8) + rows * K // 32 + 4 * K
+
+
+def cpu_baseline(w, seconds: float) -> dict:
+    """The oracle (float64 numpy) on a bounded sample: quantise a slice of the
+    activation rows and multiply it with the (pre-quantised) weight."""
+    from oracle import mx_oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    rows = min(w.M, 256)
+    xb, wb, perm = w.x_bits(rows), w.w_bits(), w.perm()
+    wq = O.quantize_mixed(wb, perm, w.split)
+    n_iter, t0 = 0, time.perf_counter()
+    while True:
+        a = O.quantize_mixed(xb, perm, w.split)
+        O.gemm_mixed(a, wq)
+        n_iter += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    tflops = 2.0 * rows * w.N * w.K * n_iter / el / 1e12
+    return {"value": tflops, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{rows} of {w.M} activation rows x full weight [{w.N},{w.K}], quantise + GEMM, "
+                      f"{n_iter} iterations in {el:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama8b_attn_2048x4096x4096")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--min-working-set-mb", type=float, default=768.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world})", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2508_02343_amd import binding as B
+    from paper_2508_02343_amd import workloads as W
+
+    w = W.BY_NAME[args.workload]
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    xb, wb, perm_np = w.x_bits(), w.w_bits(), w.perm()
+    to_bf16 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+    x0, w0 = to_bf16(xb), to_bf16(wb)
+    perm = torch.from_numpy(perm_np).to(dev)
+
+    p4, p6, p8 = w.split
+    set_bytes = (w.M * w.K * 2 + w.M * (p4 // 2 + 3 * p6 // 4 + p8 + w.K // 32)
+                 + w.N * (p4 // 2 + 3 * p6 // 4 + p8 + w.K // 32) + w.M * w.N * 2)
+    nbuf = max(1, int(np.ceil(args.min_working_set_mb * 1e6 / set_bytes)))
+    X = [x0.clone() for _ in range(nbuf)]
+    XQ = [B.MXTensor.empty(w.M, w.K, w.split, device=dev) for _ in range(nbuf)]
+    WQ = [B.MXTensor.empty(w.N, w.K, w.split, device=dev) for _ in range(nbuf)]
+    Y = [torch.empty((w.M, w.N), dtype=torch.bfloat16, device=dev) for _ in range(nbuf)]
+    del x0
+
+    stream = torch.cuda.current_stream()
+    # offline weight quantisation (once per weight), timed on its own
+    ew0, ew1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ew0.record(stream)
+    for k in range(nbuf):
+        B.quantize_weight(w0, perm, w.split, out=WQ[k], stream=stream)
+    ew1.record(stream)
+    torch.cuda.synchronize()
+    wq_ms = ew0.elapsed_time(ew1) / nbuf
+    del w0
+
+    total = args.warmup + args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(total)]
+
+    def step(i):
+        k = i % nbuf
+        e = ev[i]
+        e[0].record(stream)
+        B.quantize_act(X[k], perm, w.split, out=XQ[k], stream=stream)
+        e[1].record(stream)
+        B.gemm(XQ[k], WQ[k], y=Y[k], stream=stream)
+        e[2].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, total):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    timed = ev[args.warmup:]
+    quant_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in timed]))
+    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in timed]))
+    flops = 2.0 * w.M * w.N * w.K
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    peak = mix_peak_tflops(w.split)
+    qbytes = quant_bytes(w.M, w.K, w.split)
+    quant_gbps = qbytes / (quant_ms * 1e-3) / 1e9
+    wq_gbps = quant_bytes(w.N, w.K, w.split) / (wq_ms * 1e-3) / 1e9
+
+    out = {
+        "metric": "mixed MX GEMM TFLOPS (+quantizer GB/s) on Llama-8B/Qwen-32B layer shapes",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "mxfp4/mxfp6/mxfp8 (e2m1/e3m2/e4m3), fp32 accumulate, bf16 in/out",
+        "data": "synthetic",
+        "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "split": list(w.split),
+                   "x_dist": w.x_dist, "rotated_buffer_sets": nbuf},
+        "roofline": {"bound": "mfma", "kernel": "mixed MX GEMM", "achieved": round(gemm_tflops, 2),
+                     "peak": round(peak, 1), "unit": "TFLOP/s", "frac": round(gemm_tflops / peak, 4),
+                     "traffic": None},
+        "quantizer": {"kernel": "reorder-and-quantize (activation)", "ms": round(quant_ms, 5),
+                      "achieved": round(quant_gbps, 1), "peak": PEAK_HBM, "unit": "GB/s",
+                      "frac": round(quant_gbps / PEAK_HBM, 4), "bytes_per_launch": qbytes},
+        "gemm_ms": round(gemm_ms, 5),
+        "quant_share_of_kernel_time": round(quant_ms / (quant_ms + gemm_ms), 4),
+        "weight_quantize": {"ms": round(wq_ms, 5), "GB/s": round(wq_gbps, 1)},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,174 @@
+"""Thin ctypes binding of libmicromix.so (include/micromix.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+the library.  torch supplies device memory and the stream.  If the library
+is missing the import of this module fails loudly; there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmicromix.so")
+
+MM_OK = 0
+STATUS_NAMES = {0: "MM_OK", 1: "MM_ERR_NULL", 2: "MM_ERR_SHAPE", 3: "MM_ERR_SPLIT", 4: "MM_ERR_ALIGN",
+                5: "MM_ERR_FORMAT", 6: "MM_ERR_DEVICE"}
+
+
+class MMSplit(ctypes.Structure):
+    _fields_ = [("p4", ctypes.c_int32), ("p6", ctypes.c_int32), ("p8", ctypes.c_int32)]
+
+
+class MMTensor(ctypes.Structure):
+    _fields_ = [
+        ("rows", ctypes.c_int64),
+        ("K", ctypes.c_int64),
+        ("split", MMSplit),
+        ("q4", ctypes.c_void_p),
+        ("ld4", ctypes.c_int64),
+        ("q6", ctypes.c_void_p),
+        ("ld6", ctypes.c_int64),
+        ("q8", ctypes.c_void_p),
+        ("ld8", ctypes.c_int64),
+        ("sc", ctypes.c_void_p),
+        ("ldsc", ctypes.c_int64),
+    ]
+
+
+def _load(path: str = LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it first (python -m paper_2508_02343_amd.build_lib)")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    T = ctypes.POINTER(MMTensor)
+    lib.mm_quantize_act.argtypes = [P, I64, P, T, P]
+    lib.mm_quantize_weight.argtypes = [P, I64, P, T, P]
+    lib.mm_gemm.argtypes = [T, T, P, I64, P]
+    for f in (lib.mm_quantize_act, lib.mm_quantize_weight, lib.mm_gemm):
+        f.restype = ctypes.c_int
+    lib.mm_status_str.argtypes = [ctypes.c_int]
+    lib.mm_status_str.restype = ctypes.c_char_p
+    lib.mm_last_error.argtypes = []
+    lib.mm_last_error.restype = ctypes.c_char_p
+    lib.mm_abi_version.argtypes = []
+    lib.mm_abi_version.restype = ctypes.c_int
+    return lib
+
+
+lib = _load()
+
+
+class MMError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+def _check(status: int) -> None:
+    if status != MM_OK:
+        raise MMError(status, lib.mm_last_error().decode())
+
+
+def _round16(v: int) -> int:
+    return (v + 15) // 16 * 16
+
+
+def _stream_ptr(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+@dataclass
+class MXTensor:
+    """Quantised operand in device memory: three code buffers and scales.
+
+    Buffers are torch uint8 tensors [rows, ld] with ld rounded up to 16 bytes;
+    an empty group has no buffer.
+    """
+
+    rows: int
+    K: int
+    split: tuple[int, int, int]
+    q4: torch.Tensor | None
+    q6: torch.Tensor | None
+    q8: torch.Tensor | None
+    sc: torch.Tensor
+
+    @classmethod
+    def empty(cls, rows: int, K: int, split, device="cuda") -> "MXTensor":
+        p4, p6, p8 = (int(p) for p in split)
+
+        def buf(nbytes):
+            if nbytes == 0:
+                return None
+            return torch.empty((rows, _round16(nbytes)), dtype=torch.uint8, device=device)
+
+        return cls(rows, K, (p4, p6, p8), buf(p4 // 2), buf(3 * p6 // 4), buf(p8), buf(K // 32))
+
+    def descriptor(self) -> MMTensor:
+        d = MMTensor()
+        d.rows, d.K = self.rows, self.K
+        d.split = MMSplit(*self.split)
+        for name in ("q4", "q6", "q8", "sc"):
+            t = getattr(self, name)
+            setattr(d, name, t.data_ptr() if t is not None else None)
+            setattr(d, "ld" + name[1:], t.stride(0) if t is not None else 0)
+        return d
+
+    def host_arrays(self):
+        """Meaningful bytes of each buffer as numpy arrays (for comparisons)."""
+        import numpy as np
+
+        p4, p6, p8 = self.split
+
+        def get(t, n):
+            if t is None:
+                return np.zeros((self.rows, 0), np.uint8)
+            return t[:, :n].cpu().numpy()
+
+        return {"q4": get(self.q4, p4 // 2), "q6": get(self.q6, 3 * p6 // 4), "q8": get(self.q8, p8),
+                "sc": get(self.sc, self.K // 32)}
+
+
+def _quantize(fn, x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None, stream) -> MXTensor:
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bfloat16 tensor")
+    if perm.dtype != torch.int32 or not perm.is_contiguous():
+        raise ValueError("perm must be a contiguous int32 tensor")
+    rows, K = x.shape
+    if out is None:
+        out = MXTensor.empty(rows, K, split, device=x.device)
+    d = out.descriptor()
+    _check(fn(ctypes.c_void_p(x.data_ptr()), x.stride(0), ctypes.c_void_p(perm.data_ptr()), ctypes.byref(d),
+              _stream_ptr(stream)))
+    return out
+
+
+def quantize_act(x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None = None, stream=None) -> MXTensor:
+    """mm_quantize_act: fused reorder-and-quantize of bf16 activations."""
+    return _quantize(lib.mm_quantize_act, x, perm, split, out, stream)
+
+
+def quantize_weight(w: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None = None,
+                    stream=None) -> MXTensor:
+    """mm_quantize_weight: offline reorder-and-quantize of a bf16 weight [N, K]."""
+    return _quantize(lib.mm_quantize_weight, w, perm, split, out, stream)
+
+
+def gemm(a: MXTensor, w: MXTensor, y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """mm_gemm: Y[M, N] = A W^T in bf16 (one fp32 accumulator over all groups)."""
+    if y is None:
+        ldy = _round16(w.rows) if w.rows % 8 else w.rows
+        y = torch.empty((a.rows, ldy), dtype=torch.bfloat16, device=a.sc.device)[:, : w.rows]
+    da, dw = a.descriptor(), w.descriptor()
+    _check(lib.mm_gemm(ctypes.byref(da), ctypes.byref(dw), ctypes.c_void_p(y.data_ptr()), y.stride(0),
+                       _stream_ptr(stream)))
+    return y

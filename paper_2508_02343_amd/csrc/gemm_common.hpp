@@ -1,0 +1,117 @@
+// Shared pieces of the MicroMix mixed-precision GEMM kernels (gfx950).
+//
+// The product Y = A W^T of Sec. 2.1 eq. 1 is computed by the CDNA4
+// block-scaled MFMA V_MFMA_SCALE_F32_16X16X128_F8F6F4, which multiplies two
+// 16 x 128 operand tiles whose 32-element blocks each carry an E8M0 scale, and
+// accumulates in fp32.  All three groups (E2M1, E3M2, E4M3) feed the same
+// accumulator (Sec. 3.2 "GEMM kernel"); the format is an instruction
+// immediate, so each group runs its own specialised K loop.
+//
+// Register layout of one 16 x 128 operand tile in a wavefront (lane = 16 g + r,
+// r = tile row, g = 0..3), as measured on gfx950:
+//   E2M1 / E3M2: the lane holds the 32 elements of block g (K 32g .. 32g+31),
+//                packed densely (4 or 6 bits per element, little-endian) in
+//                the first 4 or 6 registers;
+//   E4M3:        the lane holds K 16g .. 16g+15 in bytes 0-15 and
+//                K 64+16g .. 64+16g+15 in bytes 16-31;
+//   scale:       the E8M0 byte for (row r, block b) comes from lane 16 b + r
+//                (byte 0 of the scale register with op_sel 0), for every format.
+// The fp32 result tile: lane 16 g + r, register q holds C[4 g + q][r], where
+// C's row indexes the first operand and its column the second.
+#pragma once
+
+#include "kernels.hpp"
+#include "mx_device.hpp"
+
+namespace mm {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Bytes of one 32-element block of a group.
+__host__ __device__ constexpr int block_bytes(int group) { return group == 0 ? 16 : (group == 1 ? 24 : 32); }
+
+// MFMA format selector of a group.
+__host__ __device__ constexpr int group_fmt(int group) { return group == 0 ? kE2M1 : (group == 1 ? kE3M2 : kE4M3); }
+
+// Load the 16 x 128 operand tile fragment of one lane directly from global
+// memory.  `row` is the (already clamped) operand row, `blk0` the first block
+// of this K step inside the group, `nvalid` how many of its 4 blocks exist.
+// Blocks past the group's end contribute exact zeros.
+template <int G>
+__device__ __forceinline__ v8i load_frag_global(const uint8_t* base, int64_t ld, int64_t row, int blk0, int nvalid,
+                                                int g) {
+  v8i v = {0, 0, 0, 0, 0, 0, 0, 0};
+  const uint8_t* p = base + row * ld;
+  if constexpr (G == 0) {
+    if (g < nvalid) {
+      const uint4 d = *reinterpret_cast<const uint4*>(p + (int64_t)(blk0 + g) * 16);
+      v[0] = (int)d.x;
+      v[1] = (int)d.y;
+      v[2] = (int)d.z;
+      v[3] = (int)d.w;
+    }
+  } else if constexpr (G == 1) {
+    if (g < nvalid) {
+      const uint2* s = reinterpret_cast<const uint2*>(p + (int64_t)(blk0 + g) * 24);
+      const uint2 d0 = s[0], d1 = s[1], d2 = s[2];
+      v[0] = (int)d0.x;
+      v[1] = (int)d0.y;
+      v[2] = (int)d1.x;
+      v[3] = (int)d1.y;
+      v[4] = (int)d2.x;
+      v[5] = (int)d2.y;
+    }
+  } else {
+    const uint8_t* s = p + (int64_t)blk0 * 32;
+    if ((g >> 1) < nvalid) {
+      const uint4 d = *reinterpret_cast<const uint4*>(s + 16 * g);
+      v[0] = (int)d.x;
+      v[1] = (int)d.y;
+      v[2] = (int)d.z;
+      v[3] = (int)d.w;
+    }
+    if (2 + (g >> 1) < nvalid) {
+      const uint4 d = *reinterpret_cast<const uint4*>(s + 64 + 16 * g);
+      v[4] = (int)d.x;
+      v[5] = (int)d.y;
+      v[6] = (int)d.z;
+      v[7] = (int)d.w;
+    }
+  }
+  return v;
+}
+
+// acc = acc + A(group G) x B(group G) with per-block E8M0 scales sa / sb.
+// The format selectors must reach the builtin as integer constants (they are
+// instruction immediates), hence the constexpr locals.
+#define MM_MFMA_GROUP(G, acc, a, b, sa, sb)                                                         \
+  do {                                                                                              \
+    constexpr int mm_fmt_ = group_fmt(G);                                                           \
+    (acc) = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4((a), (b), (acc), mm_fmt_, mm_fmt_, 0, \
+                                                             (sa), 0, (sb));                        \
+  } while (0)
+
+// fp32 -> bf16, round to nearest even (finite inputs; overflow gives inf).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Store lane's 4 consecutive output columns n..n+3 of row m.
+__device__ __forceinline__ void store_out4(const GemmArgs& a, int64_t m, int64_t n, const v4f& c, int64_t M,
+                                           int64_t N) {
+  if (m >= M) return;
+  uint16_t* dst = a.y + m * a.ldy + n;
+  if (n + 3 < N) {
+    const uint32_t lo = f32_to_bf16_rne(c[0]) | (f32_to_bf16_rne(c[1]) << 16);
+    const uint32_t hi = f32_to_bf16_rne(c[2]) | (f32_to_bf16_rne(c[3]) << 16);
+    *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (n + q < N) dst[q] = (uint16_t)f32_to_bf16_rne(c[q]);
+  }
+}
+
+}  // namespace mm

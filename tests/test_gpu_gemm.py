@@ -1,0 +1,116 @@
+"""GPU parity of the mixed-precision GEMM (mm_gemm) against the oracle's float64
+product of the dequantised operands, within |gpu - ref| <= 2^-8 |ref| +
+1e-3 rms(ref).  The quantised operands come from the HIP quantiser, whose
+bytes are first checked against the oracle, so both sides multiply the same
+codes."""
+
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mx_oracle as O
+from paper_2508_02343_amd import workloads as W
+from tests.gpu_helpers import assert_codes_equal, assert_gemm_close, note, to_dev_bf16, to_dev_perm, y_to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+@functools.lru_cache(maxsize=None)
+def _b():
+    from paper_2508_02343_amd import binding
+
+    return binding
+
+
+def _gpu_pair(xb, wb, perm, split):
+    b = _b()
+    p = to_dev_perm(perm)
+    a = b.quantize_act(to_dev_bf16(xb), p, split)
+    w = b.quantize_weight(to_dev_bf16(wb), p, split)
+    return a, w
+
+
+def _check_full(xb, wb, perm, split, ctx):
+    a, w = _gpu_pair(xb, wb, perm, split)
+    y = _b().gemm(a, w)
+    torch.cuda.synchronize()
+    ra, rw = O.quantize_mixed(xb, perm, split), O.quantize_mixed(wb, perm, split)
+    assert_codes_equal(a.host_arrays(), ra, ctx=ctx + " A")
+    assert_codes_equal(w.host_arrays(), rw, ctx=ctx + " W")
+    assert_gemm_close(y_to_f64(y), O.gemm_mixed(ra, rw), ctx=ctx)
+
+
+def test_tiny_config():
+    w = W.TINY
+    note(w.name)
+    _check_full(w.x_bits(), w.w_bits(), w.perm(), w.split, w.name)
+
+
+def _rand_case(M, N, split, seed):
+    K = sum(split)
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    out = rng.choice(K, max(1, K // 64), replace=False)
+    x[:, out] *= 25
+    perm = np.concatenate([np.setdiff1d(np.arange(K), out), out]).astype(np.int32)
+    wgt = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    return W.f32_to_bf16_bits(x), W.f32_to_bf16_bits(wgt), perm
+
+
+@pytest.mark.parametrize("split", [(96, 160, 96), (352, 0, 0), (0, 352, 0), (0, 0, 352), (32, 32, 288),
+                                   (128, 0, 224), (0, 64, 32)])
+@pytest.mark.parametrize("M,N", [(1, 16), (5, 70), (17, 33), (37, 130), (100, 72), (300, 260)])
+def test_ragged(M, N, split):
+    note(f"ragged M={M} N={N} split={split}")
+    xb, wb, perm = _rand_case(M, N, split, seed=M * 7 + N + split[0])
+    _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
+
+
+@pytest.mark.parametrize("w", W.decode_workloads(), ids=lambda w: w.name)
+def test_decode_configs(w):
+    """Full activation and full weight on the GPU; oracle on 256 sampled
+    weight rows (output columns), all activation rows."""
+    note(w.name)
+    xb, wb, perm = w.x_bits(), w.w_bits(), w.perm()
+    a, wq = _gpu_pair(xb, wb, perm, w.split)
+    y = _b().gemm(a, wq)
+    torch.cuda.synchronize()
+    cols = np.unique(np.concatenate([[0, w.N - 1], np.random.default_rng(2).choice(w.N, 254, replace=False)]))
+    ra, rw = O.quantize_mixed(xb, perm, w.split), O.quantize_mixed(wb[cols], perm, w.split)
+    assert_codes_equal(wq.host_arrays(), rw, rows=cols, ctx=w.name + " W")
+    assert_gemm_close(y_to_f64(y)[:, cols], O.gemm_mixed(ra, rw), ctx=w.name)
+
+
+@pytest.mark.parametrize("w", W.PREFILL, ids=lambda w: w.name)
+def test_prefill_configs_sampled(w):
+    """Full-size GEMM on the GPU; the oracle recomputes 64 x 64 sampled
+    outputs from the sampled activation and weight rows."""
+    note(w.name)
+    xb, wb, perm = w.x_bits(), w.w_bits(), w.perm()
+    a, wq = _gpu_pair(xb, wb, perm, w.split)
+    y = _b().gemm(a, wq)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([[0, w.M - 1], rng.choice(w.M, 62, replace=False)]))
+    cols = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, 62, replace=False)]))
+    ra, rw = O.quantize_mixed(xb[rows], perm, w.split), O.quantize_mixed(wb[cols], perm, w.split)
+    assert_gemm_close(y_to_f64(y[torch.from_numpy(rows).cuda()])[:, cols], O.gemm_mixed(ra, rw), ctx=w.name)
+
+
+def test_one_activation_feeds_two_weights():
+    """One quantised activation reused by two GEMMs with the same sigma."""
+    note("shared activation")
+    split = (256, 64, 64)
+    xb, wb, perm = _rand_case(40, 96, split, seed=5)
+    _, wb2, _ = _rand_case(40, 48, split, seed=6)
+    b = _b()
+    p = to_dev_perm(perm)
+    a = b.quantize_act(to_dev_bf16(xb), p, split)
+    y1 = b.gemm(a, b.quantize_weight(to_dev_bf16(wb), p, split))
+    y2 = b.gemm(a, b.quantize_weight(to_dev_bf16(wb2), p, split))
+    torch.cuda.synchronize()
+    ra = O.quantize_mixed(xb, perm, split)
+    assert_gemm_close(y_to_f64(y1), O.gemm_mixed(ra, O.quantize_mixed(wb, perm, split)), "y1")
+    assert_gemm_close(y_to_f64(y2), O.gemm_mixed(ra, O.quantize_mixed(wb2, perm, split)), "y2")
