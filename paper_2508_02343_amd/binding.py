@@ -117,10 +117,10 @@ class MXTensor:
         d = MMTensor()
         d.rows, d.K = self.rows, self.K
         d.split = MMSplit(*self.split)
-        for name in ("q4", "q6", "q8", "sc"):
+        for name, ld in (("q4", "ld4"), ("q6", "ld6"), ("q8", "ld8"), ("sc", "ldsc")):
             t = getattr(self, name)
             setattr(d, name, t.data_ptr() if t is not None else None)
-            setattr(d, "ld" + name[1:], t.stride(0) if t is not None else 0)
+            setattr(d, ld, t.stride(0) if t is not None else 0)
         return d
 
     def host_arrays(self):

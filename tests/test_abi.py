@@ -124,3 +124,13 @@ def test_gemm_rejects_mismatched_operands():
     assert b.STATUS_NAMES[_g(a, w, y=FAKE + 4)] == "MM_ERR_ALIGN"
     bad = _tensor(rows=8, split=(64, 32, 16))
     assert b.STATUS_NAMES[_g(bad, w)] == "MM_ERR_SPLIT"
+
+
+def test_binding_descriptor_fields():
+    t = b.MXTensor.empty(5, 352, (96, 160, 96), device="cpu")
+    d = t.descriptor()
+    assert (d.rows, d.K, d.split.p4, d.split.p6, d.split.p8) == (5, 352, 96, 160, 96)
+    assert (d.ld4, d.ld6, d.ld8, d.ldsc) == (48, 128, 96, 16)
+    assert d.q4 == t.q4.data_ptr() and d.sc == t.sc.data_ptr()
+    e = b.MXTensor.empty(3, 64, (64, 0, 0), device="cpu").descriptor()
+    assert e.q6 is None and e.q8 is None and e.ld6 == 0
