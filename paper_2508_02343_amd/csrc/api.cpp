@@ -14,6 +14,9 @@ namespace {
 
 constexpr int64_t kMaxQuantK = 32768;  // one row of bf16 must fit the LDS budget
 constexpr int64_t kMaxRows = (int64_t)1 << 31;
+// Up to this many activation rows the GEMM streams operands straight from
+// global memory (memory-bound decode); above it the LDS-tiled kernel runs.
+constexpr int64_t kDirectMaxM = 64;
 
 thread_local char g_err[512];
 
@@ -142,7 +145,7 @@ mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, in
   g.y = static_cast<uint16_t*>(y_bf16);
   g.ldy = ldy;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = mm::launch_gemm_direct(g, s);
+  hipError_t e = a->rows <= kDirectMaxM ? mm::launch_gemm_direct(g, s) : mm::launch_gemm_tiled(g, s);
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "mm_gemm: launch failed: %s", hipGetErrorString(e));
   return MM_OK;
 }

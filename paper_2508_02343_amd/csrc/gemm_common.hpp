@@ -28,6 +28,32 @@ namespace mm {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
+// Operand bytes past a group's last block must read as zero codes, and their
+// scales as 1.0 (E8M0 127).  Loads of such bytes are redirected to these
+// constants instead of being predicated: a predicated load is turned into a
+// branch that waits for the load to finish.
+// (Never written: plain __device__ data so that it lives in the global
+// address space and every operand load stays a global_load.)
+__device__ __attribute__((aligned(16))) uint8_t kZeroCodes[32] = {};
+__device__ uint8_t kScaleOne = 127;
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Loads through an explicit global-address-space pointer (a select between a
+// tensor pointer and kZeroCodes would otherwise become a flat load).
+__device__ __forceinline__ uint4 gload16(const void* p) {
+  const u32x4 v = *(const __attribute__((address_space(1))) u32x4*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 gload8(const void* p) {
+  const u32x2 v = *(const __attribute__((address_space(1))) u32x2*)(p);
+  return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ uint32_t gload1(const void* p) {
+  return *(const __attribute__((address_space(1))) uint8_t*)(p);
+}
+
 // Bytes of one 32-element block of a group.
 __host__ __device__ constexpr int block_bytes(int group) { return group == 0 ? 16 : (group == 1 ? 24 : 32); }
 
@@ -41,45 +67,44 @@ __host__ __device__ constexpr int group_fmt(int group) { return group == 0 ? kE2
 template <int G>
 __device__ __forceinline__ v8i load_frag_global(const uint8_t* base, int64_t ld, int64_t row, int blk0, int nvalid,
                                                 int g) {
-  v8i v = {0, 0, 0, 0, 0, 0, 0, 0};
+  v8i v;
   const uint8_t* p = base + row * ld;
   if constexpr (G == 0) {
-    if (g < nvalid) {
-      const uint4 d = *reinterpret_cast<const uint4*>(p + (int64_t)(blk0 + g) * 16);
-      v[0] = (int)d.x;
-      v[1] = (int)d.y;
-      v[2] = (int)d.z;
-      v[3] = (int)d.w;
-    }
+    const uint4 d = gload16(g < nvalid ? p + (int64_t)(blk0 + g) * 16 : kZeroCodes);
+    v[0] = (int)d.x;
+    v[1] = (int)d.y;
+    v[2] = (int)d.z;
+    v[3] = (int)d.w;
+    v[4] = v[5] = v[6] = v[7] = 0;
   } else if constexpr (G == 1) {
-    if (g < nvalid) {
-      const uint2* s = reinterpret_cast<const uint2*>(p + (int64_t)(blk0 + g) * 24);
-      const uint2 d0 = s[0], d1 = s[1], d2 = s[2];
-      v[0] = (int)d0.x;
-      v[1] = (int)d0.y;
-      v[2] = (int)d1.x;
-      v[3] = (int)d1.y;
-      v[4] = (int)d2.x;
-      v[5] = (int)d2.y;
-    }
+    const uint8_t* s = g < nvalid ? p + (int64_t)(blk0 + g) * 24 : kZeroCodes;
+    const uint2 d0 = gload8(s), d1 = gload8(s + 8), d2 = gload8(s + 16);
+    v[0] = (int)d0.x;
+    v[1] = (int)d0.y;
+    v[2] = (int)d1.x;
+    v[3] = (int)d1.y;
+    v[4] = (int)d2.x;
+    v[5] = (int)d2.y;
+    v[6] = v[7] = 0;
   } else {
     const uint8_t* s = p + (int64_t)blk0 * 32;
-    if ((g >> 1) < nvalid) {
-      const uint4 d = *reinterpret_cast<const uint4*>(s + 16 * g);
-      v[0] = (int)d.x;
-      v[1] = (int)d.y;
-      v[2] = (int)d.z;
-      v[3] = (int)d.w;
-    }
-    if (2 + (g >> 1) < nvalid) {
-      const uint4 d = *reinterpret_cast<const uint4*>(s + 64 + 16 * g);
-      v[4] = (int)d.x;
-      v[5] = (int)d.y;
-      v[6] = (int)d.z;
-      v[7] = (int)d.w;
-    }
+    const uint4 lo = gload16((g >> 1) < nvalid ? s + 16 * g : kZeroCodes);
+    const uint4 hi = gload16(2 + (g >> 1) < nvalid ? s + 64 + 16 * g : kZeroCodes);
+    v[0] = (int)lo.x;
+    v[1] = (int)lo.y;
+    v[2] = (int)lo.z;
+    v[3] = (int)lo.w;
+    v[4] = (int)hi.x;
+    v[5] = (int)hi.y;
+    v[6] = (int)hi.z;
+    v[7] = (int)hi.w;
   }
   return v;
+}
+
+// E8M0 scale of block `blk` of a row, or 1.0 past the group's end.
+__device__ __forceinline__ int load_scale(const uint8_t* row_sc, int blk, bool valid) {
+  return gload1(valid ? row_sc + blk : &kScaleOne);
 }
 
 // acc = acc + A(group G) x B(group G) with per-block E8M0 scales sa / sb.

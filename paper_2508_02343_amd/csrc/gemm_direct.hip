@@ -30,14 +30,14 @@ __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][T
       int64_t n = n0 + 16 * i + r;
       n = n < a.w.rows ? n : a.w.rows - 1;
       wf[i] = load_frag_global<G>(a.w.q[G], a.w.ld[G], n, blk0, nvalid, g);
-      ws[i] = g < nvalid ? (int)a.w.sc[n * a.w.ldsc + gblk0 + blk0 + g] : 127;
+      ws[i] = load_scale(a.w.sc + n * a.w.ldsc, gblk0 + blk0 + g, g < nvalid);
     }
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       int64_t m = m0 + 16 * j + r;
       m = m < a.x.rows ? m : a.x.rows - 1;
       xf[j] = load_frag_global<G>(a.x.q[G], a.x.ld[G], m, blk0, nvalid, g);
-      xs[j] = g < nvalid ? (int)a.x.sc[m * a.x.ldsc + gblk0 + blk0 + g] : 127;
+      xs[j] = load_scale(a.x.sc + m * a.x.ldsc, gblk0 + blk0 + g, g < nvalid);
     }
 #pragma unroll
     for (int i = 0; i < TN; ++i)
