@@ -42,7 +42,10 @@
  *   q4: row r holds p4/2 bytes at q4 + r*ld4; element 2i in the low nibble
  *       of byte i, element 2i+1 in the high nibble.
  *   q6: row r holds 3*p6/4 bytes at q6 + r*ld6; each block of 32 codes is a
- *       24-byte little-endian bit stream, code i at bits 6i..6i+5.
+ *       24-byte little-endian bit stream, code i at bits 6i..6i+5.  When
+ *       p6/32 is odd, the 8 bytes after the last block (up to the next
+ *       multiple of 16) are zero: the quantise calls write them, and
+ *       mm_gemm requires them.
  *   q8: row r holds p8 bytes at q8 + r*ld8, one code per byte.
  *   sc: row r holds K/32 E8M0 bytes (2^(byte-127)) at sc + r*ldsc, in
  *       permuted block order (E2M1 blocks first, then E3M2, then E4M3).
@@ -109,7 +112,7 @@ typedef struct {
  *           device: a non-permutation gives unspecified codes but stays in
  *           bounds only if every entry is in [0, K)).
  *   out     host descriptor of device buffers, filled as described above.
- * K may be at most 65536.  Errors: MM_ERR_NULL, MM_ERR_SHAPE, MM_ERR_SPLIT,
+ * K may be at most 32768.  Errors: MM_ERR_NULL, MM_ERR_SHAPE, MM_ERR_SPLIT,
  * MM_ERR_ALIGN, MM_ERR_DEVICE.
  */
 mm_status mm_quantize_act(const void* x_bf16, int64_t ldx, const int32_t* perm, const mm_mx_tensor* out,

@@ -1,175 +1,193 @@
-// Mixed MX GEMM for prefill shapes (many activation rows): compute-bound, so
-// operand tiles are staged through LDS and reused across the workgroup.
+// Mixed MX GEMM for prefill shapes (many activation rows): compute-bound on
+// the block-scaled MFMA, so operand tiles are staged in LDS and reused by
+// the whole workgroup.
 //
-// Workgroup tile: 128 weight rows (output columns n) x 128 activation rows
-// (output rows m); four wavefronts in a 2 x 2 grid, each owning a 64 x 64
-// output sub-tile = 4 x 4 MFMA tiles of 16 x 16 in fp32 registers.  The K
-// loop visits the E2M1 group, then E3M2, then E4M3 (Sec. 3.1 group order),
-// 128 channels (4 MX blocks) per step, all accumulating into the same
-// registers (Sec. 3.2 "GEMM kernel": one fp32 accumulation, bf16 result).
+// Workgroup tile: BN weight rows (output columns n) x BM activation rows
+// (output rows m), four wavefronts in a 2 x 2 grid, each owning a
+// (BN/2) x (BM/2) block of 16 x 16 fp32 MFMA accumulators.  The K loop visits
+// the E2M1 group, then E3M2, then E4M3 (Sec. 3.1 group order), 128 channels
+// (4 MX blocks) per step, all accumulating into the same registers
+// (Sec. 3.2 "GEMM kernel": one fp32 accumulation, one bf16 rounding).
 //
-// Per step, global -> registers -> LDS double buffering: the loads of step
-// s+1 are in flight while step s is multiplied from the other LDS buffer.
-// LDS rows are padded (80 / 112 / 144 bytes for 64 / 96 / 128 data bytes)
-// so that a wavefront's 16-byte fragment reads spread over all banks.
+// Memory pipeline (gfx950): operand bytes and their E8M0 scales go straight
+// from global memory into LDS with global_load_lds_dwordx4 / _dword, through
+// a ring of as many stages as 160 KB of LDS holds for the group's format
+// (E2M1 rows are 64 bytes per step, E3M2 96, E4M3 128), so several steps are
+// in flight while the MFMAs work on the oldest one.  Completion is tracked
+// with explicit vmcnt waits and bare s_barrier (a __syncthreads fence would
+// wait for every load in flight).  Rows are stored with a per-format chunk
+// swizzle so that a wavefront's fragment reads spread over the LDS banks.
+// Workgroups are mapped to tiles XCD by XCD and in groups of weight tiles,
+// so the tiles that run together on one XCD share its L2.
 #include "gemm_common.hpp"
 
 namespace mm {
 
 namespace tiled {
 
-constexpr int BN = 128;  // weight rows per workgroup
-constexpr int BM = 128;  // activation rows per workgroup
 constexpr int kThreads = 256;
+constexpr int kLdsBytes = 160 * 1024;
+constexpr int kRingBytes = kLdsBytes - 16;  // the last 16 bytes hold constants
+constexpr int kOneOffset = kRingBytes;      // LDS byte holding E8M0 127 (1.0)
 
 __host__ __device__ constexpr int row_bytes(int G) { return G == 0 ? 64 : (G == 1 ? 96 : 128); }
-__host__ __device__ constexpr int lds_stride(int G) { return G == 0 ? 80 : (G == 1 ? 112 : 144); }
-__host__ __device__ constexpr int chunks_per_row(int G) { return row_bytes(G) / 16; }
+__host__ __device__ constexpr int chunks(int G) { return row_bytes(G) / 16; }
 
-constexpr int kOpBytes = 128 * 144;                 // one operand tile, largest stride
-constexpr int kStageBytes = 2 * kOpBytes + 2 * 128 * 4;  // both operands + their scales
-constexpr int kLdsBytes = 2 * kStageBytes;
-
-struct Stage {
-  uint8_t* op[2];  // 0 = weight tile, 1 = activation tile
-  uint8_t* sc[2];  // [128 rows][4 blocks] E8M0 bytes per operand
+template <int G, int BN, int BM>
+struct Plan {
+  static constexpr int kRows = BN + BM;
+  static constexpr int kCodeBytes = kRows * row_bytes(G);     // codes of one stage
+  static constexpr int kStageBytes = kCodeBytes + kRows * 8;  // + 2 scale words per row
+  static constexpr int kStages = kRingBytes / kStageBytes;
+  static constexpr int kCodeLoads = kRows * chunks(G) / kThreads;  // dwordx4 DMA per thread
+  static constexpr int kScaleLoads = kRows * 2 / kThreads;         // dword DMA per thread
+  static constexpr int kLoads = kCodeLoads + kScaleLoads;
+  static_assert(kStages >= 2, "LDS ring needs two stages");
+  static_assert(kRows * chunks(G) % kThreads == 0 && kRows * 2 % kThreads == 0, "tile / thread mismatch");
+  static_assert((kStages - 2) * kLoads < 64, "vmcnt range");
 };
 
-__device__ __forceinline__ Stage stage_ptrs(uint8_t* lds, int s) {
-  Stage st;
-  uint8_t* base = lds + s * kStageBytes;
-  st.op[0] = base;
-  st.op[1] = base + kOpBytes;
-  st.sc[0] = base + 2 * kOpBytes;
-  st.sc[1] = base + 2 * kOpBytes + 512;
-  return st;
+// Physical 16-byte chunk of logical chunk c in row r (and its inverse).
+// E2M1 / E4M3 rows use an XOR swizzle; E3M2 blocks (24 bytes) straddle
+// chunks, so its rows are rotated by one chunk instead.
+template <int G>
+__device__ __forceinline__ int swz(int c, int r) {
+  if constexpr (G == 0) return c ^ ((r >> 1) & 3);
+  else if constexpr (G == 1) return ((r >> 2) & 1) ? (c == 5 ? 0 : c + 1) : c;
+  else return c ^ (r & 7);
+}
+template <int G>
+__device__ __forceinline__ int unswz(int c, int r) {
+  if constexpr (G == 1) return ((r >> 2) & 1) ? (c == 0 ? 5 : c - 1) : c;
+  else return swz<G>(c, r);
 }
 
-// Registers holding one step's global loads until they are written to LDS.
-struct Staging {
-  uint4 v[8];
-  uint32_t sc[4];  // raw scale bytes; packed only when written to LDS, so
-                   // that nothing waits for the loads before the MFMAs run
-};
+// vmcnt-only wait (expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
 
-// Operand pointers of one group, copied out of the kernel arguments (taking
-// the address of the argument block would force it into scratch memory).
-struct Ctx {
+// lgkmcnt(0) only.
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14)); }
+
+// Workgroup barrier that is also a compiler memory barrier but, unlike
+// __syncthreads, adds no wait for loads in flight.
+__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// 32-bit LDS address of a pointer into dynamic shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
+// Direct global -> LDS loads (GLOBAL_LOAD_LDS_DWORDX4 / _DWORD): lane i's 16
+// (4) bytes land at M0 + 16 i (4 i).  Written as inline asm so that the
+// compiler does not track them: it would otherwise wait for every one of them
+// before any LDS read it cannot prove disjoint, and the ring relies on the
+// explicit vmcnt waits below instead.  (M0 is not used by any other
+// instruction of these kernels.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+struct Tile {
   const uint8_t* q[2];  // weight / activation codes of the current group
   int64_t ld[2];
   const uint8_t* sc[2];
   int64_t ldsc[2];
-  int64_t row0[2];  // first weight row / activation row of this workgroup
+  int64_t row0[2];  // first weight / activation row of the tile
   int64_t rows[2];
-  int gblk0;        // first block of the group inside a scale row
+  int gblk0;        // first block of the group in a scale row
+  int nblk;         // K / 32
 };
 
-template <int G>
-__device__ __forceinline__ Ctx make_ctx(const GemmArgs& a) {
-  Ctx c;
-  c.q[0] = a.w.q[G];
-  c.q[1] = a.x.q[G];
-  c.ld[0] = a.w.ld[G];
-  c.ld[1] = a.x.ld[G];
-  c.sc[0] = a.w.sc;
-  c.sc[1] = a.x.sc;
-  c.ldsc[0] = a.w.ldsc;
-  c.ldsc[1] = a.x.ldsc;
-  c.row0[0] = (int64_t)blockIdx.x * BN;
-  c.row0[1] = (int64_t)blockIdx.y * BM;
-  c.rows[0] = a.w.rows;
-  c.rows[1] = a.x.rows;
-  c.gblk0 = G == 0 ? 0 : (G == 1 ? a.nb[0] : a.nb[0] + a.nb[1]);
-  return c;
-}
-
-template <int G>
-__device__ __forceinline__ void load_step(const Ctx& c, int blk0, int nvalid, Staging& s) {
-  constexpr int CPR = chunks_per_row(G);
+// Issue the DMA of one K step (group G, blocks blk0 .. blk0+nvalid-1) into
+// the LDS stage at `st`.
+template <int G, int BN, int BM>
+__device__ __forceinline__ void issue_step(const Tile& t, uint8_t* st, int blk0, int nvalid) {
+  using P = Plan<G, BN, BM>;
+  constexpr int CPR = chunks(G);
   constexpr int BB = block_bytes(G);
-  const int tid = threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   const int valid_bytes = nvalid * BB;
 #pragma unroll
-  for (int k = 0; k < CPR; ++k) {
-    // chunk id q = 256 k + tid over both operands; 128 * CPR = 256 * (CPR / 2)
-    // chunks per operand, so the operand index is known at compile time
-    const int op = k / (CPR / 2);
-    const int rem = kThreads * (k % (CPR / 2)) + tid;
-    const int r = rem / CPR;
-    const int ch = rem - r * CPR;
-    int64_t row = c.row0[op] + r;
-    row = row < c.rows[op] ? row : c.rows[op] - 1;
-    const uint8_t* src = c.q[op] + row * c.ld[op] + blk0 * BB + ch * 16;
-    uint4 v = gload16(ch * 16 < valid_bytes ? src : kZeroCodes);
-    if constexpr (G == 1) {
-      // an E3M2 block (24 bytes) can end in the middle of a chunk: clear the
-      // bytes past the group's end so that LDS holds zero codes there
-      const bool half = ch * 16 + 8 == valid_bytes;
-      v.z = half ? 0u : v.z;
-      v.w = half ? 0u : v.w;
-    }
-    s.v[k] = v;
-  }
-  // scales: thread t loads the 4 bytes of (operand t / 128, row t % 128)
-  {
-    // (selects, not array indexing: a lane-dependent index would put the
-    // context in scratch memory)
-    const bool op = tid >= 128;
-    const int r = tid & 127;
-    const int64_t nrows = op ? c.rows[1] : c.rows[0];
-    int64_t row = (op ? c.row0[1] : c.row0[0]) + r;
+  for (int k = 0; k < P::kCodeLoads; ++k) {
+    const int inst = wave * P::kCodeLoads + k;  // 64 consecutive 16-byte slots
+    const int q = inst * 64 + lane;
+    const bool op = q >= BN * CPR;
+    const int qq = op ? q - BN * CPR : q;
+    const int r = qq / CPR;
+    const int c = unswz<G>(qq - r * CPR, r);
+    const int64_t nrows = op ? t.rows[1] : t.rows[0];
+    int64_t row = (op ? t.row0[1] : t.row0[0]) + r;
     row = row < nrows ? row : nrows - 1;
-    const uint8_t* p = (op ? c.sc[1] : c.sc[0]) + row * (op ? c.ldsc[1] : c.ldsc[0]) + c.gblk0 + blk0;
+    const uint8_t* src = (op ? t.q[1] : t.q[0]) + row * (op ? t.ld[1] : t.ld[0]) + blk0 * BB + c * 16;
+    src = c * 16 < valid_bytes ? src : kZeroCodes;
+    dma16(src, lds_addr(st) + inst * 1024);
+  }
+  // two aligned scale words per row cover the step's four blocks
+  const int off = t.gblk0 + blk0;
+  const int a4 = off & ~3;
+  const int a4b = a4 + 4 < t.nblk ? a4 + 4 : a4;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) s.sc[j] = (uint32_t)load_scale(p, j, j < nvalid);
+  for (int k = 0; k < P::kScaleLoads; ++k) {
+    const int inst = wave * P::kScaleLoads + k;
+    const int d = inst * 64 + lane;
+    const int rr = d >> 1;
+    const bool op = rr >= BN;
+    const int r = op ? rr - BN : rr;
+    const int64_t nrows = op ? t.rows[1] : t.rows[0];
+    int64_t row = (op ? t.row0[1] : t.row0[0]) + r;
+    row = row < nrows ? row : nrows - 1;
+    const uint8_t* src = (op ? t.sc[1] : t.sc[0]) + row * (op ? t.ldsc[1] : t.ldsc[0]) + ((d & 1) ? a4b : a4);
+    dma4(src, lds_addr(st) + P::kCodeBytes + inst * 256);
   }
 }
 
+// One lane's operand fragment: tile row `row`, block g of the step.
 template <int G>
-__device__ __forceinline__ void store_step(const Stage& st, const Staging& s) {
-  constexpr int CPR = chunks_per_row(G);
-  constexpr int STR = lds_stride(G);
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int k = 0; k < CPR; ++k) {
-    const int op = k / (CPR / 2);
-    const int rem = kThreads * (k % (CPR / 2)) + tid;
-    const int r = rem / CPR;
-    const int ch = rem - r * CPR;
-    *reinterpret_cast<uint4*>(st.op[op] + r * STR + ch * 16) = s.v[k];
-  }
-  const uint32_t w = s.sc[0] | (s.sc[1] << 8) | (s.sc[2] << 16) | (s.sc[3] << 24);
-  *reinterpret_cast<uint32_t*>((tid >= 128 ? st.sc[1] : st.sc[0]) + (tid & 127) * 4) = w;
-}
-
-// One lane's fragment (row `row`, block g of the step) of a staged operand
-// tile.  Bytes of blocks past the group's end were stored as zeros, and their
-// scales as 1.0, so no masking is needed here.
-template <int G>
-__device__ __forceinline__ v8i read_frag(const uint8_t* op, int row, int g) {
-  constexpr int STR = lds_stride(G);
+__device__ __forceinline__ v8i read_frag(const uint8_t* codes, int row, int g, int r) {
+  constexpr int RB = row_bytes(G);
+  const uint8_t* p = codes + row * RB;
   v8i v;
-  const uint8_t* p = op + row * STR;
   if constexpr (G == 0) {
-    const uint4 d = *reinterpret_cast<const uint4*>(p + 16 * g);
+    const uint4 d = *reinterpret_cast<const uint4*>(p + 16 * swz<0>(g, r));
     v[0] = (int)d.x;
     v[1] = (int)d.y;
     v[2] = (int)d.z;
     v[3] = (int)d.w;
     v[4] = v[5] = v[6] = v[7] = 0;
   } else if constexpr (G == 1) {
-    const uint2* s = reinterpret_cast<const uint2*>(p + 24 * g);
-    const uint2 d0 = s[0], d1 = s[1], d2 = s[2];
-    v[0] = (int)d0.x;
-    v[1] = (int)d0.y;
-    v[2] = (int)d1.x;
-    v[3] = (int)d1.y;
-    v[4] = (int)d2.x;
-    v[5] = (int)d2.y;
+    uint2 d[3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const int b = 24 * g + 8 * j;  // logical byte of the piece
+      d[j] = *reinterpret_cast<const uint2*>(p + 16 * swz<1>(b >> 4, r) + (b & 15));
+    }
+    v[0] = (int)d[0].x;
+    v[1] = (int)d[0].y;
+    v[2] = (int)d[1].x;
+    v[3] = (int)d[1].y;
+    v[4] = (int)d[2].x;
+    v[5] = (int)d[2].y;
     v[6] = v[7] = 0;
   } else {
-    const uint4 lo = *reinterpret_cast<const uint4*>(p + 16 * g);
-    const uint4 hi = *reinterpret_cast<const uint4*>(p + 64 + 16 * g);
+    const uint4 lo = *reinterpret_cast<const uint4*>(p + 16 * swz<2>(g, r));
+    const uint4 hi = *reinterpret_cast<const uint4*>(p + 16 * swz<2>(4 + g, r));
     v[0] = (int)lo.x;
     v[1] = (int)lo.y;
     v[2] = (int)lo.z;
@@ -182,105 +200,151 @@ __device__ __forceinline__ v8i read_frag(const uint8_t* op, int row, int g) {
   return v;
 }
 
-template <int G>
-__device__ __forceinline__ void compute_step(const Stage& st, int wn0, int wm0, v4f (&acc)[4][4]) {
+template <int G, int BN, int BM>
+__device__ __forceinline__ void compute_step(const uint8_t* st, const uint8_t* one, int off, int nvalid, int wn0,
+                                             int wm0, v4f (&acc)[BN / 32][BM / 32]) {
+  using P = Plan<G, BN, BM>;
+  constexpr int TN = BN / 32, TM = BM / 32;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, r = lane & 15;
-  v8i wf[4], xf[4];
-  int ws[4], xs[4];
+  const uint8_t* sc = st + P::kCodeBytes + (off & 3) + g;  // this lane's block in a scale row
+  // blocks past the group's end read the constant 1.0 instead (an address
+  // select keeps the read unconditional)
+  const bool sc_ok = g < nvalid;
+  v8i xf[TM];
+  int xs[TM];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int j = 0; j < TM; ++j) {
+    const int row = BN + wm0 + 16 * j + r;
+    xf[j] = read_frag<G>(st, row, g, r);
+    xs[j] = *(sc_ok ? sc + row * 8 : one);
+  }
+#pragma unroll
+  for (int i = 0; i < TN; ++i) {
     const int row = wn0 + 16 * i + r;
-    wf[i] = read_frag<G>(st.op[0], row, g);
-    ws[i] = st.sc[0][row * 4 + g];
+    const v8i wf = read_frag<G>(st, row, g, r);
+    const int ws = *(sc_ok ? sc + row * 8 : one);
+#pragma unroll
+    for (int j = 0; j < TM; ++j) MM_MFMA_GROUP(G, acc[i][j], wf, xf[j], ws, xs[j]);
   }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = wm0 + 16 * j + r;
-    xf[j] = read_frag<G>(st.op[1], row, g);
-    xs[j] = st.sc[1][row * 4 + g];
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) MM_MFMA_GROUP(G, acc[i][j], wf[i], xf[j], ws[i], xs[j]);
 }
 
-// All K steps of one group, double-buffered through LDS.  `stage` is the LDS
-// buffer the group starts in; it is left pointing at the next free buffer.
-template <int G>
-__device__ __forceinline__ void run_group(const GemmArgs& a, uint8_t* lds, int& stage, int wn0, int wm0,
-                                          v4f (&acc)[4][4]) {
+template <int G, int BN, int BM>
+__device__ __forceinline__ void run_group(const GemmArgs& a, uint8_t* lds, int64_t n0, int64_t m0, int wn0,
+                                          int wm0, v4f (&acc)[BN / 32][BM / 32]) {
+  using P = Plan<G, BN, BM>;
+  constexpr int NS = P::kStages;
   const int nb = a.nb[G];
   if (nb == 0) return;
+  Tile t;
+  t.q[0] = a.w.q[G];
+  t.q[1] = a.x.q[G];
+  t.ld[0] = a.w.ld[G];
+  t.ld[1] = a.x.ld[G];
+  t.sc[0] = a.w.sc;
+  t.sc[1] = a.x.sc;
+  t.ldsc[0] = a.w.ldsc;
+  t.ldsc[1] = a.x.ldsc;
+  t.row0[0] = n0;
+  t.row0[1] = m0;
+  t.rows[0] = a.w.rows;
+  t.rows[1] = a.x.rows;
+  t.gblk0 = G == 0 ? 0 : (G == 1 ? a.nb[0] : a.nb[0] + a.nb[1]);
+  t.nblk = a.nb[0] + a.nb[1] + a.nb[2];
   const int S = (nb + 3) >> 2;
-  const Ctx c = make_ctx<G>(a);
-  Staging stg;
-  load_step<G>(c, 0, nb < 4 ? nb : 4, stg);
-  store_step<G>(stage_ptrs(lds, stage), stg);
-  __syncthreads();
-  // steady state: no branches inside, so the scheduler keeps the order
-  // global loads (step ks+1) -> MFMAs (step ks) -> LDS writes (step ks+1)
-  for (int ks = 0; ks + 1 < S; ++ks) {
-    const int left = nb - 4 * (ks + 1);
-    load_step<G>(c, 4 * (ks + 1), left < 4 ? left : 4, stg);
-    compute_step<G>(stage_ptrs(lds, stage), wn0, wm0, acc);
-    // keep the LDS writes (which wait for the global loads) behind the
-    // MFMAs, so the loads' latency overlaps the matrix work
-    __builtin_amdgcn_sched_barrier(0);
-    store_step<G>(stage_ptrs(lds, stage ^ 1), stg);
-    __syncthreads();
-    stage ^= 1;
+  auto nval = [&](int s) { return nb - 4 * s < 4 ? nb - 4 * s : 4; };
+
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < S) issue_step<G, BN, BM>(t, lds + p * P::kStageBytes, 4 * p, nval(p));
+
+  for (int s = 0; s < S; ++s) {
+    // steps s+1 .. s+NS-2 may still be in flight; step s must have landed
+    if (s + NS - 2 < S) wait_vmcnt<(NS - 2) * P::kLoads>();
+    else wait_vmcnt<0>();
+    barrier();  // everyone's step-s data is in LDS; everyone is done with step s-1
+    // refill the stage that step s-1 used, then multiply step s
+    const int sn = s + NS - 1;
+    if (sn < S) issue_step<G, BN, BM>(t, lds + (sn % NS) * P::kStageBytes, 4 * sn, nval(sn));
+    compute_step<G, BN, BM>(lds + (s % NS) * P::kStageBytes, lds + kOneOffset, t.gblk0 + 4 * s, nval(s), wn0,
+                            wm0, acc);
   }
-  compute_step<G>(stage_ptrs(lds, stage), wn0, wm0, acc);
-  __syncthreads();
-  stage ^= 1;
+  // the next group lays its stages out differently: every wave must be done
+  // reading this group's LDS first
+  wait_lgkm0();
+  barrier();
 }
 
 }  // namespace tiled
 
 using namespace tiled;
 
-__global__ __launch_bounds__(kThreads) void gemm_tiled_kernel(GemmArgs a) {
-  extern __shared__ __align__(16) uint8_t lds[];
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6;
-  const int wn0 = (wave & 1) * 64;   // wave's weight-row offset in the tile
-  const int wm0 = (wave >> 1) * 64;  // wave's activation-row offset
-  const int64_t n_base = (int64_t)blockIdx.x * BN;
-  const int64_t m_base = (int64_t)blockIdx.y * BM;
+template <int BN, int BM>
+__global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int tiles_n, int tiles_m) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+  constexpr int TN = BN / 32, TM = BM / 32;
+  constexpr int kGroupN = 4;  // weight tiles that share an XCD's L2 at a time
 
-  v4f acc[4][4];
+  // workgroup -> tile: consecutive tiles per XCD (workgroups are dealt to the
+  // 8 XCDs round-robin), then groups of kGroupN weight tiles, activation
+  // tiles fastest inside a group
+  const int T = tiles_n * tiles_m;
+  const int wg = blockIdx.x;
+  const int xcd = wg & 7, k = wg >> 3;
+  const int per = T >> 3, extra = T & 7;
+  const int t = xcd * per + (xcd < extra ? xcd : extra) + k;
+  const int grp = t / (kGroupN * tiles_m);
+  const int within = t - grp * kGroupN * tiles_m;
+  const int gn = tiles_n - grp * kGroupN < kGroupN ? tiles_n - grp * kGroupN : kGroupN;
+  const int tn = grp * kGroupN + within % gn;
+  const int tm = within / gn;
+  const int64_t n0 = (int64_t)tn * BN, m0 = (int64_t)tm * BM;
+
+  const int wave = threadIdx.x >> 6;
+  const int wn0 = (wave & 1) * (BN / 2);
+  const int wm0 = (wave >> 1) * (BM / 2);
+
+  v4f acc[TN][TM];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TM; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+  if (threadIdx.x == 0) lds[kOneOffset] = 127;  // seen after the first barrier
 
-  int stage = 0;
-  run_group<0>(a, lds, stage, wn0, wm0, acc);
-  run_group<1>(a, lds, stage, wn0, wm0, acc);
-  run_group<2>(a, lds, stage, wn0, wm0, acc);
+  run_group<0, BN, BM>(a, lds, n0, m0, wn0, wm0, acc);
+  run_group<1, BN, BM>(a, lds, n0, m0, wn0, wm0, acc);
+  run_group<2, BN, BM>(a, lds, n0, m0, wn0, wm0, acc);
 
-  const int lane = tid & 63;
+  const int lane = threadIdx.x & 63;
   const int g = lane >> 4, r = lane & 15;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      store_out4(a, m_base + wm0 + 16 * j + r, n_base + wn0 + 16 * i + 4 * g, acc[i][j], a.x.rows, a.w.rows);
+    for (int j = 0; j < TM; ++j)
+      store_out4(a, m0 + wm0 + 16 * j + r, n0 + wn0 + 16 * i + 4 * g, acc[i][j], a.x.rows, a.w.rows);
 }
 
-hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t stream) {
+template <int BN, int BM>
+static hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel<BN, BM>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const dim3 grid((unsigned)((a.w.rows + BN - 1) / BN), (unsigned)((a.x.rows + BM - 1) / BM));
-  hipLaunchKernelGGL(gemm_tiled_kernel, grid, dim3(kThreads), kLdsBytes, stream, a);
+  const int tn = (int)((a.w.rows + BN - 1) / BN), tm = (int)((a.x.rows + BM - 1) / BM);
+  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM>), dim3((unsigned)(tn * tm)), dim3(kThreads), kLdsBytes, stream, a,
+                     tn, tm);
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t stream) {
+  // 256 x 256 tiles when they still give every CU several tiles, else
+  // 256 x 128 so that the grid covers the 256 CUs
+  const int64_t tiles_big = ((a.w.rows + 255) / 256) * ((a.x.rows + 255) / 256);
+  if (tiles_big >= 768) return launch_tile<256, 256>(a, stream);
+  return launch_tile<256, 128>(a, stream);
 }
 
 }  // namespace mm

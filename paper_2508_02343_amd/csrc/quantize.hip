@@ -97,6 +97,13 @@ __global__ __launch_bounds__(1024) void quantize_rows_kernel(QuantArgs a, int R)
         d32[0] = w0;
         d32[1] = w1;
         d32[2] = w2;
+        // An odd number of E3M2 blocks ends the row 8 bytes short of a 16-byte
+        // boundary; those padding bytes are part of the layout and read as
+        // zero codes by the GEMM's 16-byte loads.
+        if (half == 1 && blk - a.nb4 == a.nb6 - 1 && (a.nb6 & 1)) {
+          d32[3] = 0u;
+          d32[4] = 0u;
+        }
       } else {
         uint32_t w[4] = {0, 0, 0, 0};
 #pragma unroll

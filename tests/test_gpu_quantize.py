@@ -133,3 +133,22 @@ def test_full_size_weight_sampled_rows():
     got = _run(wb, perm, w.split, weight=True)
     rows = np.unique(np.concatenate([[0, w.N - 1], np.random.default_rng(1).choice(w.N, 62, replace=False)]))
     assert_codes_equal(got, O.quantize_mixed(wb[rows], perm, w.split), rows=rows, ctx=w.name + " W")
+
+
+@pytest.mark.parametrize("p6", [32, 96, 160])
+def test_e3m2_row_padding_is_zero(p6):
+    """With an odd number of E3M2 blocks the 8 bytes after the last block are
+    written as zeros (part of the packed layout the GEMM reads)."""
+    split = (64, p6, 32)
+    K = sum(split)
+    note(f"E3M2 padding p6={p6}")
+    rng = np.random.default_rng(p6)
+    bits = W.f32_to_bf16_bits(rng.standard_normal((9, K)).astype(np.float32))
+    b = _b()
+    out = b.MXTensor.empty(9, K, split)
+    out.q6.fill_(0xAB)
+    b.quantize_act(to_dev_bf16(bits), to_dev_perm(np.arange(K, dtype=np.int32)), split, out=out)
+    torch.cuda.synchronize()
+    q6 = out.q6.cpu().numpy()
+    n = 3 * p6 // 4
+    assert np.all(q6[:, n:n + 8] == 0)
