@@ -117,6 +117,21 @@ __device__ __forceinline__ int load_scale(const uint8_t* row_sc, int blk, bool v
                                                              (sa), 0, (sb));                        \
   } while (0)
 
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// The 32 x 32 x 64 form (V_MFMA_SCALE_F32_32X32X64_F8F6F4): lane 32 g + r
+// holds row r; E2M1 / E3M2 lanes hold block g of the 64-channel step, E4M3
+// lanes hold channels 16g .. 16g+15 and 32+16g .. 32+16g+15; the scale of
+// (row r, block b) comes from lane 32 b + r.  Result: lane 32 g + r,
+// register q holds C[8 (q/4) + 4 g + q%4][r].  On gfx950 this form runs E2M1
+// and E3M2 well above the 16 x 16 x 128 form's rate.
+#define MM_MFMA32_GROUP(G, acc, a, b, sa, sb)                                                       \
+  do {                                                                                              \
+    constexpr int mm_fmt_ = group_fmt(G);                                                           \
+    (acc) = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4((a), (b), (acc), mm_fmt_, mm_fmt_, 0,  \
+                                                            (sa), 0, (sb));                         \
+  } while (0)
+
 // fp32 -> bf16, round to nearest even (finite inputs; overflow gives inf).
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   const uint32_t u = __float_as_uint(f);

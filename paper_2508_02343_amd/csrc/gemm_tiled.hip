@@ -101,6 +101,20 @@ __device__ __forceinline__ void dma4(const void* src, uint32_t lds) {
                : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
                : "memory", "m0");
 }
+// Same loads with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// offset, which keeps the per-step address arithmetic scalar.
+__device__ __forceinline__ void dma16_s(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4_s(uint32_t voff, const void* sbase, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 struct Tile {
@@ -158,14 +172,80 @@ __device__ __forceinline__ void issue_step(const Tile& t, uint8_t* st, int blk0,
   }
 }
 
-// One lane's operand fragment: tile row `row`, block g of the step.
+// Loop-invariant part of a thread's DMA addresses for one group: the byte
+// offset of each of its chunks (row * ld + chunk * 16) and scale words
+// (row * ldsc + 4 * word) relative to the operand's base pointer.
+template <int G, int BN, int BM>
+struct DmaPlan {
+  using P = Plan<G, BN, BM>;
+  uint32_t code[P::kCodeLoads];
+  uint32_t scale[P::kScaleLoads];
+};
+
+template <int G, int BN, int BM>
+__device__ __forceinline__ DmaPlan<G, BN, BM> make_plan(const Tile& t, int wave) {
+  using P = Plan<G, BN, BM>;
+  constexpr int CPR = chunks(G);
+  const int lane = threadIdx.x & 63;
+  DmaPlan<G, BN, BM> d;
+#pragma unroll
+  for (int k = 0; k < P::kCodeLoads; ++k) {
+    const int q = (wave * P::kCodeLoads + k) * 64 + lane;
+    const bool op = q >= BN * CPR;
+    const int qq = op ? q - BN * CPR : q;
+    const int r = qq / CPR;
+    const int c = unswz<G>(qq - r * CPR, r);
+    const int64_t nrows = op ? t.rows[1] : t.rows[0];
+    int64_t row = (op ? t.row0[1] : t.row0[0]) + r;
+    row = row < nrows ? row : nrows - 1;
+    d.code[k] = (uint32_t)(row * (op ? t.ld[1] : t.ld[0])) + c * 16;
+  }
+#pragma unroll
+  for (int k = 0; k < P::kScaleLoads; ++k) {
+    const int dd = (wave * P::kScaleLoads + k) * 64 + lane;
+    const int rr = dd >> 1;
+    const bool op = rr >= BN;
+    const int r = op ? rr - BN : rr;
+    const int64_t nrows = op ? t.rows[1] : t.rows[0];
+    int64_t row = (op ? t.row0[1] : t.row0[0]) + r;
+    row = row < nrows ? row : nrows - 1;
+    d.scale[k] = (uint32_t)(row * (op ? t.ldsc[1] : t.ldsc[0])) + 4 * (dd & 1);
+  }
+  return d;
+}
+
+// DMA of a full step (four valid blocks whose two scale words lie inside the
+// scale row): scalar base pointers, precomputed per-lane offsets.
+template <int G, int BN, int BM>
+__device__ __forceinline__ void issue_full_step(const Tile& t, const DmaPlan<G, BN, BM>& d, uint32_t st, int wave,
+                                                int blk0) {
+  using P = Plan<G, BN, BM>;
+  constexpr int CPR = chunks(G);
+  constexpr int BB = block_bytes(G);
+#pragma unroll
+  for (int k = 0; k < P::kCodeLoads; ++k) {
+    const int inst = wave * P::kCodeLoads + k;
+    const bool op = inst * 64 >= BN * CPR;  // uniform: an instruction never spans operands
+    dma16_s(d.code[k], (op ? t.q[1] : t.q[0]) + blk0 * BB, st + inst * 1024);
+  }
+  const int a4 = (t.gblk0 + blk0) & ~3;
+#pragma unroll
+  for (int k = 0; k < P::kScaleLoads; ++k) {
+    const int inst = wave * P::kScaleLoads + k;
+    const bool op = inst * 32 >= BN;
+    dma4_s(d.scale[k], (op ? t.sc[1] : t.sc[0]) + a4, st + P::kCodeBytes + inst * 256);
+  }
+}
+
+// One lane's operand fragment for the 32 x 32 x 64 MFMA: tile row `row`,
+// 64-channel half kk of the step, lane half g.
 template <int G>
-__device__ __forceinline__ v8i read_frag(const uint8_t* codes, int row, int g, int r) {
+__device__ __forceinline__ v8i read_frag(const uint8_t* codes, int row, int kk, int g, int r) {
   constexpr int RB = row_bytes(G);
   const uint8_t* p = codes + row * RB;
   v8i v;
   if constexpr (G == 0) {
-    const uint4 d = *reinterpret_cast<const uint4*>(p + 16 * swz<0>(g, r));
+    const uint4 d = *reinterpret_cast<const uint4*>(p + 16 * swz<0>(2 * kk + g, r));
     v[0] = (int)d.x;
     v[1] = (int)d.y;
     v[2] = (int)d.z;
@@ -175,7 +255,7 @@ __device__ __forceinline__ v8i read_frag(const uint8_t* codes, int row, int g, i
     uint2 d[3];
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
-      const int b = 24 * g + 8 * j;  // logical byte of the piece
+      const int b = 24 * (2 * kk + g) + 8 * j;  // logical byte of the piece
       d[j] = *reinterpret_cast<const uint2*>(p + 16 * swz<1>(b >> 4, r) + (b & 15));
     }
     v[0] = (int)d[0].x;
@@ -186,8 +266,8 @@ __device__ __forceinline__ v8i read_frag(const uint8_t* codes, int row, int g, i
     v[5] = (int)d[2].y;
     v[6] = v[7] = 0;
   } else {
-    const uint4 lo = *reinterpret_cast<const uint4*>(p + 16 * swz<2>(g, r));
-    const uint4 hi = *reinterpret_cast<const uint4*>(p + 16 * swz<2>(4 + g, r));
+    const uint4 lo = *reinterpret_cast<const uint4*>(p + 16 * swz<2>(4 * kk + g, r));
+    const uint4 hi = *reinterpret_cast<const uint4*>(p + 16 * swz<2>(4 * kk + 2 + g, r));
     v[0] = (int)lo.x;
     v[1] = (int)lo.y;
     v[2] = (int)lo.z;
@@ -200,38 +280,56 @@ __device__ __forceinline__ v8i read_frag(const uint8_t* codes, int row, int g, i
   return v;
 }
 
+template <int BN, int BM>
+using Acc = v16f[BN / 64][BM / 64];
+
 template <int G, int BN, int BM>
 __device__ __forceinline__ void compute_step(const uint8_t* st, const uint8_t* one, int off, int nvalid, int wn0,
-                                             int wm0, v4f (&acc)[BN / 32][BM / 32]) {
+                                             int wm0, Acc<BN, BM>& acc) {
   using P = Plan<G, BN, BM>;
-  constexpr int TN = BN / 32, TM = BM / 32;
+  constexpr int TN = BN / 64, TM = BM / 64;  // 32-row fragments per wave
   const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15;
+  const int g = lane >> 5, r = lane & 31;
   const uint8_t* sc = st + P::kCodeBytes + (off & 3) + g;  // this lane's block in a scale row
   // blocks past the group's end read the constant 1.0 instead (an address
   // select keeps the read unconditional)
-  const bool sc_ok = g < nvalid;
-  v8i xf[TM];
-  int xs[TM];
+  v8i xf[2][TM];
+  int xs[2][TM];
 #pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int row = BN + wm0 + 16 * j + r;
-    xf[j] = read_frag<G>(st, row, g, r);
-    xs[j] = *(sc_ok ? sc + row * 8 : one);
+  for (int kk = 0; kk < 2; ++kk) {
+    const bool ok = 2 * kk + g < nvalid;
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int row = BN + wm0 + 32 * j + r;
+      xf[kk][j] = read_frag<G>(st, row, kk, g, r);
+      xs[kk][j] = *(ok ? sc + row * 8 + 2 * kk : one);
+    }
   }
+  // weight fragments are double-buffered: the next one is read while the
+  // MFMAs of the current one run
+  v8i wf = read_frag<G>(st, wn0 + r, 0, g, r);
+  int ws = *(g < nvalid ? sc + (wn0 + r) * 8 : one);
 #pragma unroll
-  for (int i = 0; i < TN; ++i) {
-    const int row = wn0 + 16 * i + r;
-    const v8i wf = read_frag<G>(st, row, g, r);
-    const int ws = *(sc_ok ? sc + row * 8 : one);
+  for (int t = 0; t < 2 * TN; ++t) {
+    const int kk = t / TN, i = t % TN;
+    v8i wn = wf;
+    int wsn = ws;
+    if (t + 1 < 2 * TN) {
+      const int kn = (t + 1) / TN, in = (t + 1) % TN;
+      const int row = wn0 + 32 * in + r;
+      wn = read_frag<G>(st, row, kn, g, r);
+      wsn = *(2 * kn + g < nvalid ? sc + row * 8 + 2 * kn : one);
+    }
 #pragma unroll
-    for (int j = 0; j < TM; ++j) MM_MFMA_GROUP(G, acc[i][j], wf, xf[j], ws, xs[j]);
+    for (int j = 0; j < TM; ++j) MM_MFMA32_GROUP(G, acc[i][j], wf, xf[kk][j], ws, xs[kk][j]);
+    wf = wn;
+    ws = wsn;
   }
 }
 
 template <int G, int BN, int BM>
-__device__ __forceinline__ void run_group(const GemmArgs& a, uint8_t* lds, int64_t n0, int64_t m0, int wn0,
-                                          int wm0, v4f (&acc)[BN / 32][BM / 32]) {
+__device__ __forceinline__ void run_group(const GemmArgs& a, uint8_t* lds, int64_t n0, int64_t m0, int wave,
+                                          int wn0, int wm0, Acc<BN, BM>& acc) {
   using P = Plan<G, BN, BM>;
   constexpr int NS = P::kStages;
   const int nb = a.nb[G];
@@ -253,10 +351,22 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint8_t* lds, int64
   t.nblk = a.nb[0] + a.nb[1] + a.nb[2];
   const int S = (nb + 3) >> 2;
   auto nval = [&](int s) { return nb - 4 * s < 4 ? nb - 4 * s : 4; };
+  const DmaPlan<G, BN, BM> plan = make_plan<G, BN, BM>(t, wave);
+  const uint32_t lds0 = lds_addr(lds);
+  // full steps take the scalar-address path; a group's last partial step
+  // (and a step whose second scale word would pass the row end) the general one
+  auto issue = [&](int s) {
+    const int b0 = 4 * s;
+    uint8_t* st = lds + (s % NS) * P::kStageBytes;
+    if (nval(s) == 4 && ((t.gblk0 + b0) & ~3) + 4 < t.nblk)
+      issue_full_step<G, BN, BM>(t, plan, lds0 + (s % NS) * P::kStageBytes, wave, b0);
+    else
+      issue_step<G, BN, BM>(t, st, b0, nval(s));
+  };
 
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
-    if (p < S) issue_step<G, BN, BM>(t, lds + p * P::kStageBytes, 4 * p, nval(p));
+    if (p < S) issue(p);
 
   for (int s = 0; s < S; ++s) {
     // steps s+1 .. s+NS-2 may still be in flight; step s must have landed
@@ -265,7 +375,7 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint8_t* lds, int64
     barrier();  // everyone's step-s data is in LDS; everyone is done with step s-1
     // refill the stage that step s-1 used, then multiply step s
     const int sn = s + NS - 1;
-    if (sn < S) issue_step<G, BN, BM>(t, lds + (sn % NS) * P::kStageBytes, 4 * sn, nval(sn));
+    if (sn < S) issue(sn);
     compute_step<G, BN, BM>(lds + (s % NS) * P::kStageBytes, lds + kOneOffset, t.gblk0 + 4 * s, nval(s), wn0,
                             wm0, acc);
   }
@@ -282,7 +392,6 @@ using namespace tiled;
 template <int BN, int BM>
 __global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int tiles_n, int tiles_m) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
-  constexpr int TN = BN / 32, TM = BM / 32;
   constexpr int kGroupN = 4;  // weight tiles that share an XCD's L2 at a time
 
   // workgroup -> tile: consecutive tiles per XCD (workgroups are dealt to the
@@ -300,28 +409,36 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int
   const int tm = within / gn;
   const int64_t n0 = (int64_t)tn * BN, m0 = (int64_t)tm * BM;
 
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: keeps DMA setup scalar
   const int wn0 = (wave & 1) * (BN / 2);
   const int wm0 = (wave >> 1) * (BM / 2);
 
-  v4f acc[TN][TM];
+  Acc<BN, BM> acc;
 #pragma unroll
-  for (int i = 0; i < TN; ++i)
+  for (int i = 0; i < BN / 64; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < BM / 64; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
   if (threadIdx.x == 0) lds[kOneOffset] = 127;  // seen after the first barrier
 
-  run_group<0, BN, BM>(a, lds, n0, m0, wn0, wm0, acc);
-  run_group<1, BN, BM>(a, lds, n0, m0, wn0, wm0, acc);
-  run_group<2, BN, BM>(a, lds, n0, m0, wn0, wm0, acc);
+  run_group<0, BN, BM>(a, lds, n0, m0, wave, wn0, wm0, acc);
+  run_group<1, BN, BM>(a, lds, n0, m0, wave, wn0, wm0, acc);
+  run_group<2, BN, BM>(a, lds, n0, m0, wave, wn0, wm0, acc);
 
+  // lane 32 g + r, register q: output column n = 8 (q/4) + 4 g + q%4 of the
+  // fragment, output row m = r
   const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15;
+  const int g = lane >> 5, r = lane & 31;
 #pragma unroll
-  for (int i = 0; i < TN; ++i)
+  for (int i = 0; i < BN / 64; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j)
-      store_out4(a, m0 + wm0 + 16 * j + r, n0 + wn0 + 16 * i + 4 * g, acc[i][j], a.x.rows, a.w.rows);
+    for (int j = 0; j < BM / 64; ++j)
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const v4f c = {acc[i][j][4 * h], acc[i][j][4 * h + 1], acc[i][j][4 * h + 2], acc[i][j][4 * h + 3]};
+        store_out4(a, m0 + wm0 + 32 * j + r, n0 + wn0 + 32 * i + 8 * h + 4 * g, c, a.x.rows, a.w.rows);
+      }
 }
 
 template <int BN, int BM>
