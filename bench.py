@@ -49,6 +49,35 @@ def quant_bytes(rows: int, K: int, split) -> int:
     return rows * K * 2 + rows * (p4 // 2 + 3 * p6 // 4 + p8) + rows * K // 32 + 4 * K
 
 
+GEMM_SOURCES = ("gemm_tiled.hip", "gemm_direct.hip", "gemm_common.hpp", "mx_device.hpp", "kernels.hpp", "api.cpp")
+CALIB_BYTES = 256 << 20  # plain copy used to calibrate the FETCH_SIZE / WRITE_SIZE counters
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2508_02343_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per GEMM launch from the committed rocprofv3 counter summary,
+    or None when the summary is missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    entry = rec.get(workload)
+    if not entry or entry.get("source_hash") != gemm_source_hash():
+        return None
+    return entry.get("hbm_bytes_per_launch")
+
+
 def cpu_baseline(w, seconds: float) -> dict:
     """The oracle (float64 numpy) on a bounded sample: quantise a slice of the
     activation rows and multiply it with the (pre-quantised) weight."""
@@ -118,6 +147,12 @@ def main() -> int:
     del x0
 
     stream = torch.cuda.current_stream()
+    # a plain device copy of known size: under rocprofv3 --pmc its FETCH_SIZE /
+    # WRITE_SIZE give the scale factor for the GEMM's counters
+    calib = torch.empty(CALIB_BYTES, dtype=torch.uint8, device=dev)
+    calib_dst = torch.empty_like(calib)
+    calib_dst.copy_(calib)
+    del calib, calib_dst
     # offline weight quantisation (once per weight), timed on its own
     ew0, ew1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ew0.record(stream)
@@ -128,31 +163,38 @@ def main() -> int:
     wq_ms = ew0.elapsed_time(ew1) / nbuf
     del w0
 
-    total = args.warmup + args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(total)]
-
     def step(i):
         k = i % nbuf
-        e = ev[i]
-        e[0].record(stream)
         B.quantize_act(X[k], perm, w.split, out=XQ[k], stream=stream)
-        e[1].record(stream)
         B.gemm(XQ[k], WQ[k], y=Y[k], stream=stream)
-        e[2].record(stream)
+
+    def timed(fn, n):
+        """Average duration of n back-to-back launches, HIP events on the
+        stream the kernels run on."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(n):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.warmup, total):
+    for i in range(args.steps):
         step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
+    # per-kernel average launch durations: each kernel alone, back to back over
+    # the same rotated buffers (no event between launches)
+    quant_ms = timed(lambda i: B.quantize_act(X[i % nbuf], perm, w.split, out=XQ[i % nbuf], stream=stream),
+                     args.steps)
+    gemm_ms = timed(lambda i: B.gemm(XQ[i % nbuf], WQ[i % nbuf], y=Y[i % nbuf], stream=stream), args.steps)
+
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    timed = ev[args.warmup:]
-    quant_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in timed]))
-    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in timed]))
     flops = 2.0 * w.M * w.N * w.K
     value = flops / (ms_per_step * 1e-3) / 1e12
     gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
@@ -178,7 +220,7 @@ def main() -> int:
                    "x_dist": w.x_dist, "rotated_buffer_sets": nbuf},
         "roofline": {"bound": "mfma", "kernel": "mixed MX GEMM", "achieved": round(gemm_tflops, 2),
                      "peak": round(peak, 1), "unit": "TFLOP/s", "frac": round(gemm_tflops / peak, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic(w.name), "source_hash": gemm_source_hash()},
         "quantizer": {"kernel": "reorder-and-quantize (activation)", "ms": round(quant_ms, 5),
                       "achieved": round(quant_gbps, 1), "peak": PEAK_HBM, "unit": "GB/s",
                       "frac": round(quant_gbps / PEAK_HBM, 4), "bytes_per_launch": qbytes},
