@@ -3,134 +3,278 @@
 // sigma (Sec. 3.1), takes each 32-channel block's shared E8M0 scale and writes
 // E2M1 / E3M2 / E4M3 codes for the three groups (Sec. 2.1 MX rule).
 //
-// Memory-bound design for gfx950:
-//  - a workgroup owns R consecutive rows; the rows are streamed into LDS with
-//    16-byte coalesced loads (the only HBM read);
-//  - each thread owns a fixed run of 16 permuted channels (half a block) and
-//    keeps its 16 sigma entries in registers for all R rows, so sigma is read
-//    once per workgroup;
-//  - the gather is a read from LDS; the block absmax is a max over the
-//    thread's 16 values and one cross-lane exchange with the neighbour lane
-//    that owns the other half of the block;
-//  - codes are packed in registers and written with one 8-, 12- or 16-byte
-//    store per thread, so a wavefront writes a contiguous span of each group.
+// HBM-bound design for gfx950:
+//  - a workgroup owns `rpp` rows per pass and `npass` passes; one thread per
+//    (row, 32-channel block), so each thread always quantises the same block
+//    index and keeps that block's 32 sigma entries in registers, as LDS byte
+//    addresses, for the whole workgroup;
+//  - rows arrive with 16-byte coalesced loads (the only HBM read) into
+//    registers and are written to one of two LDS stages: the loads of pass
+//    p+1 are in flight while pass p is quantised from the other stage;
+//  - the gather is 32 LDS u16 reads per thread; the block absmax is a packed
+//    16-bit max over the sign-cleared bf16 bits;
+//  - the codes come from the gfx950 scaled conversions, which divide by the
+//    E8M0 scale and round to nearest even (E2M1 and E4M3 two codes per
+//    instruction, E3M2 one instruction per block giving the packed 24-byte bit
+//    stream).  The E4M3 conversion does not saturate, so E4M3 inputs are first
+//    clamped to 448 * scale, which is exact in bf16;
+//  - consecutive lanes own consecutive blocks, so a wavefront's code stores
+//    cover a contiguous span of each group.
 #include "kernels.hpp"
-#include "mx_device.hpp"
 
 namespace mm {
+namespace {
 
-__global__ __launch_bounds__(1024) void quantize_rows_kernel(QuantArgs a, int R) {
-  extern __shared__ uint16_t lds_rows[];  // [R][K]
-  const int tid = threadIdx.x;
-  const int T = blockDim.x;
-  const int64_t row0 = (int64_t)blockIdx.x * R;
-  const int K = a.K;
-  const int nrows = (int)((a.rows - row0) < R ? (a.rows - row0) : R);
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x32 __attribute__((ext_vector_type(32)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef int i32x6 __attribute__((ext_vector_type(6)));
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-  // 1. stream the rows into LDS (16 B per load, fully coalesced)
-  const int chunks_per_row = K >> 3;
-  const int total_chunks = nrows * chunks_per_row;
-  for (int c = tid; c < total_chunks; c += T) {
-    const int r = c / chunks_per_row;
-    const int j = c - r * chunks_per_row;
-    const uint4 v = *reinterpret_cast<const uint4*>(a.x + (row0 + r) * a.ldx + (int64_t)j * 8);
-    *reinterpret_cast<uint4*>(lds_rows + r * K + j * 8) = v;
-  }
-  __syncthreads();
+// The second LDS stage sits at a fixed byte offset, so stage selection folds
+// into the immediate offset of the LDS reads.  One stage holds at most this
+// many bytes (rpp * K * 2).
+constexpr int kStageOff = 32768;
+constexpr int kMaxChunks = 4;  // 16-byte loads per thread per pass
 
-  // 2. every thread handles 16 permuted channels per row
-  const int units = K >> 4;
-  for (int u = tid; u < units; u += T) {
-    int p[16];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int4 v = *reinterpret_cast<const int4*>(a.perm + u * 16 + q * 4);
-      p[4 * q + 0] = v.x;
-      p[4 * q + 1] = v.y;
-      p[4 * q + 2] = v.z;
-      p[4 * q + 3] = v.w;
-    }
-    // an out-of-range entry (a caller error) must not read outside the row
-#pragma unroll
-    for (int i = 0; i < 16; ++i) p[i] = (unsigned)p[i] < (unsigned)K ? p[i] : 0;
-    const int blk = u >> 1;
-    const int half = u & 1;
-    const int group = blk < a.nb4 ? 0 : (blk < a.nb4 + a.nb6 ? 1 : 2);
-    const FmtParams f = fmt_params(group);
+// LDS pointers built from 32-bit byte addresses (the base already added)
+typedef const __attribute__((address_space(3))) uint16_t lds_u16_t;
 
-    for (int r = 0; r < nrows; ++r) {
-      const uint16_t* src = lds_rows + r * K;
-      uint32_t h[16];
-      uint32_t amax = 0;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        h[i] = src[p[i]];
-        const uint32_t m = h[i] & 0x7FFFu;
-        amax = m > amax ? m : amax;
-      }
-      // the other half of this block lives in the neighbouring lane
-      const uint32_t other = (uint32_t)__shfl_xor((int)amax, 1);
-      amax = other > amax ? other : amax;
-      const int e = block_exponent(amax, f.emax);
-      const int64_t row = row0 + r;
-
-      if (group == 0) {
-        uint32_t w0 = 0, w1 = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) w0 |= encode_bf16(h[i], e, f) << (4 * i);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) w1 |= encode_bf16(h[8 + i], e, f) << (4 * i);
-        uint8_t* dst = a.q4 + row * a.ld4 + (int64_t)blk * 16 + half * 8;
-        *reinterpret_cast<uint2*>(dst) = make_uint2(w0, w1);
-      } else if (group == 1) {
-        // 16 six-bit codes = 96 bits: a little-endian bit stream
-        uint32_t c[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) c[i] = encode_bf16(h[i], e, f);
-        const uint32_t w0 = c[0] | (c[1] << 6) | (c[2] << 12) | (c[3] << 18) | (c[4] << 24) | (c[5] << 30);
-        const uint32_t w1 =
-            (c[5] >> 2) | (c[6] << 4) | (c[7] << 10) | (c[8] << 16) | (c[9] << 22) | (c[10] << 28);
-        const uint32_t w2 = (c[10] >> 4) | (c[11] << 2) | (c[12] << 8) | (c[13] << 14) | (c[14] << 20) |
-                            (c[15] << 26);
-        uint8_t* dst = a.q6 + row * a.ld6 + (int64_t)(blk - a.nb4) * 24 + half * 12;
-        uint32_t* d32 = reinterpret_cast<uint32_t*>(dst);
-        d32[0] = w0;
-        d32[1] = w1;
-        d32[2] = w2;
-        // An odd number of E3M2 blocks ends the row 8 bytes short of a 16-byte
-        // boundary; those padding bytes are part of the layout and read as
-        // zero codes by the GEMM's 16-byte loads.
-        if (half == 1 && blk - a.nb4 == a.nb6 - 1 && (a.nb6 & 1)) {
-          d32[3] = 0u;
-          d32[4] = 0u;
-        }
-      } else {
-        uint32_t w[4] = {0, 0, 0, 0};
-#pragma unroll
-        for (int i = 0; i < 16; ++i) w[i >> 2] |= encode_bf16(h[i], e, f) << (8 * (i & 3));
-        uint8_t* dst = a.q8 + row * a.ld8 + (int64_t)(blk - a.nb4 - a.nb6) * 32 + half * 16;
-        *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-      if (half == 0) a.sc[row * a.ldsc + blk] = (uint8_t)(e + 127);
-    }
-  }
+__device__ __forceinline__ uint16_t lds_u16(uint32_t byte_addr) {
+  return *reinterpret_cast<lds_u16_t*>((uintptr_t)byte_addr);
 }
 
-// Rows per workgroup: enough to amortise the sigma load, while keeping the
-// LDS footprint near 32 KB so several workgroups stay resident per CU.
-static int rows_per_block(int K) {
-  int R = 16384 / K;
-  return R < 1 ? 1 : (R > 4 ? 4 : R);
+__device__ __forceinline__ uint32_t max_u16x2(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t,
+                            __builtin_elementwise_max(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
+}
+
+__device__ __forceinline__ uint32_t min_u16x2(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t,
+                            __builtin_elementwise_min(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
+}
+
+// Quantise one 32-channel block of one row from LDS stage kStage.
+template <int kStage>
+__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, const QuantArgs& a,
+                                               int64_t row, int blk) {
+  // gather: the block's 32 permuted channels as 16 packed bf16 pairs
+  uint32_t d[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    u16x2 v;
+    v.x = lds_u16(addr[2 * i] + kStage * kStageOff);
+    v.y = lds_u16(addr[2 * i + 1] + kStage * kStageOff);
+    d[i] = __builtin_bit_cast(uint32_t, v);
+  }
+
+  // absmax: bf16 magnitudes compare as unsigned integers
+  uint32_t m[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) m[i] = d[i] & 0x7FFF7FFFu;
+#pragma unroll
+  for (int s = 8; s >= 1; s >>= 1)
+#pragma unroll
+    for (int i = 0; i < s; ++i) m[i] = max_u16x2(m[i], m[i + s]);
+  const uint32_t amax = (m[0] & 0xFFFFu) > (m[0] >> 16) ? (m[0] & 0xFFFFu) : (m[0] >> 16);
+
+  // Shared exponent e = floor(log2 amax) - emax, clamped below at -127: for
+  // a bf16 amax with biased exponent E this is max(E - 127 - emax, -127); a
+  // subnormal or zero amax (E = 0) lands on the clamp.  The E8M0 byte is e+127.
+  const int emax = group == 0 ? 2 : (group == 1 ? 4 : 8);
+  const int E = (int)(amax >> 7);
+  const uint32_t sbyte = (uint32_t)(E - emax > 0 ? E - emax : 0);
+  // the conversions read the scale's E8M0 exponent from an fp32 operand
+  const float scale = __uint_as_float(sbyte << 23);
+
+  if (group == 0) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t v = 0;
+      v = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(v, __builtin_bit_cast(bf16x2, d[4 * q + 0]), scale, 0);
+      v = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(v, __builtin_bit_cast(bf16x2, d[4 * q + 1]), scale, 1);
+      v = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(v, __builtin_bit_cast(bf16x2, d[4 * q + 2]), scale, 2);
+      v = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(v, __builtin_bit_cast(bf16x2, d[4 * q + 3]), scale, 3);
+      w[q] = v;
+    }
+    *reinterpret_cast<uint4*>(a.q4 + row * a.ld4 + (int64_t)blk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else if (group == 1) {
+    u32x16 v;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = d[i];
+    const i32x6 c = __builtin_amdgcn_cvt_scalef32_pk32_bf6_bf16(__builtin_bit_cast(bf16x32, v), scale);
+    const int b6 = blk - a.nb4;
+    uint2* dst = reinterpret_cast<uint2*>(a.q6 + row * a.ld6 + (int64_t)b6 * 24);
+    dst[0] = make_uint2((uint32_t)c[0], (uint32_t)c[1]);
+    dst[1] = make_uint2((uint32_t)c[2], (uint32_t)c[3]);
+    dst[2] = make_uint2((uint32_t)c[4], (uint32_t)c[5]);
+    // An odd number of E3M2 blocks ends the row 8 bytes short of a 16-byte
+    // boundary; those padding bytes are part of the layout and read as zero
+    // codes by the GEMM's 16-byte loads.
+    if (b6 == a.nb6 - 1 && (a.nb6 & 1)) dst[3] = make_uint2(0u, 0u);
+  } else {
+    // 448 * 2^e in bf16: biased exponent e + 127 + 8 = sbyte + 8, mantissa 0x60
+    const uint32_t lim = ((sbyte + 8u) << 7) | 0x60u;
+    const uint32_t lim2 = lim | (lim << 16);
+    uint32_t w[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      // clamp the magnitudes, keep the signs (bitfield insert)
+      const uint32_t c0 = min_u16x2(d[2 * q] & 0x7FFF7FFFu, lim2) | (d[2 * q] & 0x80008000u);
+      const uint32_t c1 = min_u16x2(d[2 * q + 1] & 0x7FFF7FFFu, lim2) | (d[2 * q + 1] & 0x80008000u);
+      i16x2 v = {0, 0};
+      v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c0), scale, false);
+      v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c1), scale, true);
+      w[q] = __builtin_bit_cast(uint32_t, v);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(a.q8 + row * a.ld8 + (int64_t)(blk - a.nb4 - a.nb6) * 32);
+    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+  }
+  a.sc[row * a.ldsc + blk] = (uint8_t)sbyte;
+}
+
+}  // namespace
+
+// Launch shape: blockDim.x = roundup64(rpp * nblk) <= kMaxThreads threads;
+// thread t owns pass-row t / nblk and block t % nblk.  kPipe: two LDS stages
+// of rpp * K * 2 <= kStageOff bytes, loads of the next pass overlap the
+// current one; otherwise npass == 1 and one stage of up to 2 * kStageOff.
+template <int kMaxThreads, bool kPipe>
+__global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a, int rpp, int npass) {
+  extern __shared__ u32x4 lds4[];
+  const int tid = threadIdx.x;
+  const int T = blockDim.x;
+  const int K = a.K;
+  const int nblk = K >> 5;
+  const int prow = tid / nblk;
+  const int blk = tid - prow * nblk;
+  const bool active = prow < rpp;
+  const int stage_bytes = rpp * K * 2;
+  const int nchunks = stage_bytes >> 4;  // 16-byte chunks per pass
+  if (!kPipe) npass = 1;
+  const int64_t row_first = (int64_t)blockIdx.x * rpp * npass;
+
+  // sigma of this thread's block as LDS byte addresses within a stage; an
+  // out-of-range entry (a caller error) is clamped to stay inside the row
+  uint32_t addr[32];
+  const int base = (int)(uint32_t)(uintptr_t)lds4 + (active ? prow : 0) * K * 2;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int4 v = *reinterpret_cast<const int4*>(a.perm + (active ? blk : 0) * 32 + 4 * q);
+    const int p[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) addr[4 * q + i] = (uint32_t)(base + 2 * ((unsigned)p[i] < (unsigned)K ? p[i] : 0));
+  }
+  // keep the full addresses in registers: otherwise the common base is
+  // factored out and re-added before every LDS read
+#pragma unroll
+  for (int i = 0; i < 32; ++i) asm volatile("" : "+v"(addr[i]));
+  const int group = blk < a.nb4 ? 0 : (blk < a.nb4 + a.nb6 ? 1 : 2);
+
+  // 16-byte chunk c of a pass lies in pass-row c / (K/8); rows past the end
+  // are read from the last row (their results are never stored) and chunks
+  // past the pass go to a 16-byte dummy slot after the stages, so every load
+  // and LDS write is unconditional and in bounds
+  const int chunks_per_row = K >> 3;
+  const uint32_t dummy = (uint32_t)((kPipe ? kStageOff : 0) + stage_bytes);
+  u32x4 buf[kMaxChunks];
+#define MM_LOAD_PASS(P)                                                                              \
+  {                                                                                                  \
+    const int64_t r0_ = row_first + (int64_t)(P)*rpp;                                                \
+    _Pragma("unroll") for (int j = 0; j < kMaxChunks; ++j) {                                         \
+      int c = tid + j * T;                                                                           \
+      c = c < nchunks ? c : nchunks - 1;                                                             \
+      const int r = c / chunks_per_row;                                                              \
+      int64_t row = r0_ + r;                                                                         \
+      row = row < a.rows ? row : a.rows - 1;                                                         \
+      buf[j] = *reinterpret_cast<const u32x4*>(a.x + row * a.ldx + (int64_t)(c - r * chunks_per_row) * 8); \
+    }                                                                                                \
+  }
+#define MM_STORE_PASS(STAGE)                                                                         \
+  {                                                                                                  \
+    _Pragma("unroll") for (int j = 0; j < kMaxChunks; ++j) {                                         \
+      const int c = tid + j * T;                                                                     \
+      const uint32_t off = c < nchunks ? (uint32_t)((STAGE)*kStageOff + c * 16) : dummy;            \
+      lds4[off >> 4] = buf[j];                                                                       \
+    }                                                                                                \
+  }
+
+  MM_LOAD_PASS(0);
+  MM_STORE_PASS(0);
+  __syncthreads();
+  for (int p = 0; p < npass; ++p) {
+    const bool more = kPipe && p + 1 < npass;
+    if (more) MM_LOAD_PASS(p + 1);
+    const int64_t row = row_first + (int64_t)p * rpp + prow;
+    if (active && row < a.rows) {
+      if ((p & 1) == 0)
+        quantize_block<0>(addr, group, a, row, blk);
+      else
+        quantize_block<1>(addr, group, a, row, blk);
+    }
+    if (more) MM_STORE_PASS((p + 1) & 1);
+    __syncthreads();
+  }
+#undef MM_LOAD_PASS
+#undef MM_STORE_PASS
+}
+
+// Allow more than 64 KB of dynamic LDS (two 32 KB stages plus the dummy
+// slot, or one 64 KB row).
+template <int kMaxThreads, bool kPipe>
+static hipError_t allow_lds(size_t bytes) {
+  static bool done = false;
+  if (done || bytes <= 65536) return hipSuccess;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(quantize_rows_kernel<kMaxThreads, kPipe>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kStageOff + 16);
+  if (e == hipSuccess) done = true;
+  return e;
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
-  const int R = rows_per_block(a.K);
-  const int units = a.K >> 4;
-  int T = ((units + 63) / 64) * 64;
-  if (T > 1024) T = 1024;
-  const int64_t grid = (a.rows + R - 1) / R;
-  const size_t lds = (size_t)R * a.K * sizeof(uint16_t);
-  hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)grid), dim3(T), lds, stream, a, R);
+  if (a.rows == 0) return hipSuccess;
+  const int K = a.K;
+  const int nblk = K >> 5;
+  // A row wider than one stage (K > 16384) is quantised without overlap, one
+  // row per workgroup of K/32 threads (up to 1024).
+  if (K * 2 > kStageOff) {
+    const int T = (nblk + 63) / 64 * 64;
+    const size_t lds = (size_t)K * 2 + 16;
+    hipError_t e = allow_lds<1024, false>(lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((quantize_rows_kernel<1024, false>), dim3((unsigned)a.rows), dim3(T), lds, stream, a, 1, 1);
+    return hipGetLastError();
+  }
+  // rows per pass: the fewest idle lanes (ties: more rows) among launches of
+  // up to 512 threads, stopping at the first of at least 256 threads; a pass
+  // must fit one LDS stage
+  const int max_rpp = kStageOff / (K * 2);
+  int rpp = 1;
+  double best = 2.0;
+  for (int r = 1; r <= max_rpp && r * nblk <= 512; ++r) {
+    const int t = (r * nblk + 63) / 64 * 64;
+    const double idle = (double)(t - r * nblk) / t;
+    if (idle <= best) {
+      best = idle;
+      rpp = r;
+    }
+    if (t >= 256) break;
+  }
+  const int T = (rpp * nblk + 63) / 64 * 64;
+  const int64_t passes = (a.rows + rpp - 1) / rpp;
+  // about 1024 workgroups (4 per CU), each running npass passes
+  int npass = (int)(passes / 1024);
+  npass = npass < 1 ? 1 : (npass > 16 ? 16 : npass);
+  const int64_t grid = (passes + npass - 1) / npass;
+  // two stages plus the 16-byte dummy slot
+  const size_t lds = (size_t)kStageOff + (size_t)rpp * K * 2 + 16;
+  hipError_t e = allow_lds<512, true>(lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((quantize_rows_kernel<512, true>), dim3((unsigned)grid), dim3(T), lds, stream, a, rpp, npass);
   return hipGetLastError();
 }
 
