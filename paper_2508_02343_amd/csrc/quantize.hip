@@ -4,10 +4,11 @@
 // E2M1 / E3M2 / E4M3 codes for the three groups (Sec. 2.1 MX rule).
 //
 // HBM-bound design for gfx950:
-//  - a workgroup owns `rpp` rows per pass and `npass` passes; one thread per
-//    (row, 32-channel block), so each thread always quantises the same block
-//    index and keeps that block's 32 sigma entries in registers, as LDS byte
-//    addresses, for the whole workgroup;
+//  - a pass is `rpp` consecutive rows; the grid is sized to the number of
+//    workgroups the chip holds at once and workgroup g takes passes g,
+//    g + grid, ...; one thread per (row, 32-channel block), so each thread
+//    always quantises the same block index and keeps that block's 32 sigma
+//    entries in registers, as LDS byte addresses, for the whole workgroup;
 //  - rows arrive with 16-byte coalesced loads (the only HBM read) into
 //    registers and are written to one of two LDS stages: the loads of pass
 //    p+1 are in flight while pass p is quantised from the other stage;
@@ -140,11 +141,12 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
 }  // namespace
 
 // Launch shape: blockDim.x = roundup64(rpp * nblk) <= kMaxThreads threads;
-// thread t owns pass-row t / nblk and block t % nblk.  kPipe: two LDS stages
-// of rpp * K * 2 <= kStageOff bytes, loads of the next pass overlap the
-// current one; otherwise npass == 1 and one stage of up to 2 * kStageOff.
+// thread t owns pass-row t / nblk and block t % nblk; gridDim.x <= number of
+// passes.  kPipe: two LDS stages of rpp * K * 2 <= kStageOff bytes, loads of
+// the next pass overlap the current one; otherwise gridDim.x equals the
+// number of passes and one stage holds up to 2 * kStageOff bytes.
 template <int kMaxThreads, bool kPipe>
-__global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a, int rpp, int npass) {
+__global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a, int rpp) {
   extern __shared__ u32x4 lds4[];
   const int tid = threadIdx.x;
   const int T = blockDim.x;
@@ -155,8 +157,8 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   const bool active = prow < rpp;
   const int stage_bytes = rpp * K * 2;
   const int nchunks = stage_bytes >> 4;  // 16-byte chunks per pass
-  if (!kPipe) npass = 1;
-  const int64_t row_first = (int64_t)blockIdx.x * rpp * npass;
+  const int64_t passes = (a.rows + rpp - 1) / rpp;
+  const int64_t stride = gridDim.x;
 
   // sigma of this thread's block as LDS byte addresses within a stage; an
   // out-of-range entry (a caller error) is clamped to stay inside the row
@@ -184,7 +186,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   u32x4 buf[kMaxChunks];
 #define MM_LOAD_PASS(P)                                                                              \
   {                                                                                                  \
-    const int64_t r0_ = row_first + (int64_t)(P)*rpp;                                                \
+    const int64_t r0_ = (int64_t)(P)*rpp;                                                            \
     _Pragma("unroll") for (int j = 0; j < kMaxChunks; ++j) {                                         \
       int c = tid + j * T;                                                                           \
       c = c < nchunks ? c : nchunks - 1;                                                             \
@@ -203,20 +205,21 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
     }                                                                                                \
   }
 
-  MM_LOAD_PASS(0);
+  int64_t q = blockIdx.x;
+  MM_LOAD_PASS(q);
   MM_STORE_PASS(0);
   __syncthreads();
-  for (int p = 0; p < npass; ++p) {
-    const bool more = kPipe && p + 1 < npass;
-    if (more) MM_LOAD_PASS(p + 1);
-    const int64_t row = row_first + (int64_t)p * rpp + prow;
+  for (int i = 0; q < passes; ++i, q += stride) {
+    const bool more = kPipe && q + stride < passes;
+    if (more) MM_LOAD_PASS(q + stride);
+    const int64_t row = q * rpp + prow;
     if (active && row < a.rows) {
-      if ((p & 1) == 0)
+      if ((i & 1) == 0)
         quantize_block<0>(addr, group, a, row, blk);
       else
         quantize_block<1>(addr, group, a, row, blk);
     }
-    if (more) MM_STORE_PASS((p + 1) & 1);
+    if (more) MM_STORE_PASS((i + 1) & 1);
     __syncthreads();
   }
 #undef MM_LOAD_PASS
@@ -235,6 +238,29 @@ static hipError_t allow_lds(size_t bytes) {
   return e;
 }
 
+// Workgroups of the pipelined kernel resident on the current device at once
+// (per-CU occupancy times CU count), cached per thread for the last shape.
+static hipError_t resident_workgroups(int T, size_t lds, int* cap) {
+  thread_local int last_dev = -1, last_T = 0, last_cap = 0;
+  thread_local size_t last_lds = 0;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev != last_dev || T != last_T || lds != last_lds) {
+    int per_cu = 0, cus = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_rows_kernel<512, true>, T, lds);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    last_dev = dev;
+    last_T = T;
+    last_lds = lds;
+    last_cap = (per_cu < 1 ? 1 : per_cu) * (cus < 1 ? 1 : cus);
+  }
+  *cap = last_cap;
+  return hipSuccess;
+}
+
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
   if (a.rows == 0) return hipSuccess;
   const int K = a.K;
@@ -246,7 +272,7 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
     const size_t lds = (size_t)K * 2 + 16;
     hipError_t e = allow_lds<1024, false>(lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((quantize_rows_kernel<1024, false>), dim3((unsigned)a.rows), dim3(T), lds, stream, a, 1, 1);
+    hipLaunchKernelGGL((quantize_rows_kernel<1024, false>), dim3((unsigned)a.rows), dim3(T), lds, stream, a, 1);
     return hipGetLastError();
   }
   // rows per pass: the fewest idle lanes (ties: more rows) among launches of
@@ -266,15 +292,16 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
   }
   const int T = (rpp * nblk + 63) / 64 * 64;
   const int64_t passes = (a.rows + rpp - 1) / rpp;
-  // about 1024 workgroups (4 per CU), each running npass passes
-  int npass = (int)(passes / 1024);
-  npass = npass < 1 ? 1 : (npass > 16 ? 16 : npass);
-  const int64_t grid = (passes + npass - 1) / npass;
   // two stages plus the 16-byte dummy slot
   const size_t lds = (size_t)kStageOff + (size_t)rpp * K * 2 + 16;
   hipError_t e = allow_lds<512, true>(lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((quantize_rows_kernel<512, true>), dim3((unsigned)grid), dim3(T), lds, stream, a, rpp, npass);
+  // one wave of workgroups: as many as the chip holds at once
+  int cap = 0;
+  e = resident_workgroups(T, lds, &cap);
+  if (e != hipSuccess) return e;
+  const int64_t grid = passes < cap ? passes : cap;
+  hipLaunchKernelGGL((quantize_rows_kernel<512, true>), dim3((unsigned)grid), dim3(T), lds, stream, a, rpp);
   return hipGetLastError();
 }
 
