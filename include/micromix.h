@@ -39,22 +39,36 @@
  * X'[:, j] = X[:, sigma[j]].  Channels [0, p4) are E2M1, [p4, p4+p6) are
  * E3M2 and [p4+p6, K) are E4M3.  Each row's blocks of 32 consecutive permuted
  * channels share one scale; a block never straddles two groups.
- *   q4: row r holds p4/2 bytes at q4 + r*ld4; element 2i in the low nibble
- *       of byte i, element 2i+1 in the high nibble.
- *   q6: row r holds 3*p6/4 bytes at q6 + r*ld6; each block of 32 codes is a
- *       24-byte little-endian bit stream, code i at bits 6i..6i+5.  When
- *       p6/32 is odd, the 8 bytes after the last block (up to the next
- *       multiple of 16) are zero: the quantise calls write them, and
- *       mm_gemm requires them.
- *   q8: row r holds p8 bytes at q8 + r*ld8, one code per byte.
- *   sc: row r holds K/32 E8M0 bytes (2^(byte-127)) at sc + r*ldsc, in
- *       permuted block order (E2M1 blocks first, then E3M2, then E4M3).
+ *
+ * The packed layout is laid out for the GEMM's loads (it plays the role of the
+ * tensor-core scale-factor layout the paper's quantisation kernel writes):
+ *   R   = rows rounded up to a multiple of 32 (a "row group" is 32 rows);
+ *   nbG = pG / 32 blocks of group G, SG = ceil(nbG / 4) "steps" of 4 blocks;
+ *   RBG = bytes of one row's step: 64 (E2M1), 96 (E3M2), 128 (E4M3).
+ * Codes of group G: SG steps, each R * RBG bytes; inside a step, row group q
+ * (rows 32q .. 32q+31) occupies 32 * RBG bytes starting at q * 32 * RBG, and
+ * within it, for row r = row % 32 and block j = 0..3 of the step:
+ *   E2M1: block j of row r at  j * 512 + r * 16  (16 bytes: element 2i in
+ *         the low nibble of byte i, 2i+1 in the high nibble);
+ *   E3M2: block j of row r at  j * 768 + r * 24  (24 bytes: a little-endian
+ *         bit stream, element i at bits 6i .. 6i+5);
+ *   E4M3: bytes 16h .. 16h+15 (h = 0, 1) of block j of row r at
+ *         (2j + h) * 512 + r * 16  (one code per byte).
+ * So block b of row n of group G starts at byte
+ *   (b/4) * R * RBG + (n/32) * 32 * RBG + [offset above with j = b%4, r = n%32].
+ * Scales: (S4 + S6 + S8) steps numbered t (E2M1 steps first, then E3M2, then
+ * E4M3); byte (t * R + row) * 4 + j is the E8M0 scale (2^(byte-127)) of block
+ * j of that step of that row.
+ * Padding: blocks past the end of a group inside its last step, and rows
+ * rows .. R-1, hold zero codes and scale byte 0; the quantise calls write
+ * them and mm_gemm relies on them.
  * Element codes are sign | exponent | mantissa with the OCP MX encodings:
  * E2M1 bias 1, E3M2 bias 3, E4M3 bias 7 (S.1111.111 is NaN and never written).
+ * mm_mx_layout_sizes() gives each buffer's byte count.
  * Requirements: K > 0 and K % 32 == 0; p4, p6, p8 >= 0, each % 32 == 0,
- * p4 + p6 + p8 == K; every non-empty buffer pointer 16-byte aligned; each
- * ld* a multiple of 16 and >= the row's byte count rounded up to 16.  A
- * buffer of an empty group (p == 0) may be NULL and its ld is ignored.
+ * p4 + p6 + p8 == K; every buffer of a non-empty group 16-byte aligned and
+ * at least the size mm_mx_layout_sizes() reports; a buffer of an empty group
+ * (p == 0) may be NULL.
  *
  * Quantisation rule (bit-exact): for a block with largest magnitude amax the
  * scale exponent is e = floor(log2 amax) - emax, with emax the format's top
@@ -73,7 +87,7 @@
 extern "C" {
 #endif
 
-#define MM_ABI_VERSION 1
+#define MM_ABI_VERSION 2
 
 typedef enum {
   MM_OK = 0,
@@ -93,15 +107,22 @@ typedef struct {
   int64_t rows;   /* M for activations, N for weights            */
   int64_t K;      /* channels per row                            */
   mm_split split; /* group sizes, identical for a and w in GEMM  */
-  uint8_t* q4;
-  int64_t ld4; /* bytes between rows of q4 */
-  uint8_t* q6;
-  int64_t ld6; /* bytes between rows of q6 */
-  uint8_t* q8;
-  int64_t ld8; /* bytes between rows of q8 */
-  uint8_t* sc;
-  int64_t ldsc; /* bytes between rows of sc */
+  uint8_t* q4;    /* E2M1 codes (layout above)                    */
+  uint8_t* q6;    /* E3M2 codes                                   */
+  uint8_t* q8;    /* E4M3 codes                                   */
+  uint8_t* sc;    /* E8M0 scales                                  */
 } mm_mx_tensor;
+
+typedef struct {
+  int64_t q4, q6, q8, sc; /* bytes of each buffer */
+} mm_mx_sizes;
+
+/*
+ * Byte counts of the four buffers of a quantised tensor of `rows` rows with
+ * this K and split (layout above).  Host-only arithmetic, no device access.
+ * Errors: MM_ERR_NULL (out is NULL), MM_ERR_SHAPE, MM_ERR_SPLIT.
+ */
+mm_status mm_mx_layout_sizes(int64_t rows, int64_t K, mm_split split, mm_mx_sizes* out);
 
 /*
  * Fused reorder-and-quantize of activations (Sec. 3.2 "Quantization kernel";
@@ -111,7 +132,8 @@ typedef struct {
  *   perm    device, int32 [K], a permutation of [0, K) (not checked on the
  *           device: a non-permutation gives unspecified codes but stays in
  *           bounds only if every entry is in [0, K)).
- *   out     host descriptor of device buffers, filled as described above.
+ *   out     host descriptor of device buffers, filled as described above
+ *           (including the padding).
  * K may be at most 32768.  Errors: MM_ERR_NULL, MM_ERR_SHAPE, MM_ERR_SPLIT,
  * MM_ERR_ALIGN, MM_ERR_DEVICE.
  */
@@ -137,7 +159,7 @@ mm_status mm_quantize_weight(const void* w_bf16, int64_t ldw, const int32_t* per
  *   w       weight descriptor, rows = N; same K and split as a.
  *   y_bf16  device, bf16 [M, N] row-major, row stride ldy elements
  *           (ldy >= N, ldy % 8 == 0, 16-byte aligned).
- * Errors: MM_ERR_NULL, MM_ERR_SHAPE (K or split differ, ld too small),
+ * Errors: MM_ERR_NULL, MM_ERR_SHAPE (K or split differ, ldy below N),
  * MM_ERR_SPLIT, MM_ERR_ALIGN, MM_ERR_DEVICE.
  */
 mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, int64_t ldy, void* stream);

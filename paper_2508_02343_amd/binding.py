@@ -31,14 +31,14 @@ class MMTensor(ctypes.Structure):
         ("K", ctypes.c_int64),
         ("split", MMSplit),
         ("q4", ctypes.c_void_p),
-        ("ld4", ctypes.c_int64),
         ("q6", ctypes.c_void_p),
-        ("ld6", ctypes.c_int64),
         ("q8", ctypes.c_void_p),
-        ("ld8", ctypes.c_int64),
         ("sc", ctypes.c_void_p),
-        ("ldsc", ctypes.c_int64),
     ]
+
+
+class MMSizes(ctypes.Structure):
+    _fields_ = [("q4", ctypes.c_int64), ("q6", ctypes.c_int64), ("q8", ctypes.c_int64), ("sc", ctypes.c_int64)]
 
 
 def _load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -59,6 +59,8 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mm_last_error.restype = ctypes.c_char_p
     lib.mm_abi_version.argtypes = []
     lib.mm_abi_version.restype = ctypes.c_int
+    lib.mm_mx_layout_sizes.argtypes = [I64, I64, MMSplit, ctypes.POINTER(MMSizes)]
+    lib.mm_mx_layout_sizes.restype = ctypes.c_int
     return lib
 
 
@@ -80,6 +82,13 @@ def _round16(v: int) -> int:
     return (v + 15) // 16 * 16
 
 
+def layout_sizes(rows: int, K: int, split) -> dict:
+    """mm_mx_layout_sizes: byte count of each buffer of a quantised tensor."""
+    sz = MMSizes()
+    _check(lib.mm_mx_layout_sizes(rows, K, MMSplit(*(int(p) for p in split)), ctypes.byref(sz)))
+    return {"q4": sz.q4, "q6": sz.q6, "q8": sz.q8, "sc": sz.sc}
+
+
 def _stream_ptr(stream) -> ctypes.c_void_p:
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -88,11 +97,9 @@ def _stream_ptr(stream) -> ctypes.c_void_p:
 
 @dataclass
 class MXTensor:
-    """Quantised operand in device memory: three code buffers and scales.
-
-    Buffers are torch uint8 tensors [rows, ld] with ld rounded up to 16 bytes;
-    an empty group has no buffer.
-    """
+    """Quantised operand in device memory: three code buffers and scales,
+    each a flat uint8 tensor in the packed layout of include/micromix.h
+    (an empty group has no buffer)."""
 
     rows: int
     K: int
@@ -104,38 +111,31 @@ class MXTensor:
 
     @classmethod
     def empty(cls, rows: int, K: int, split, device="cuda") -> "MXTensor":
-        p4, p6, p8 = (int(p) for p in split)
+        split = tuple(int(p) for p in split)
+        sz = layout_sizes(rows, K, split)
 
         def buf(nbytes):
             if nbytes == 0:
                 return None
-            return torch.empty((rows, _round16(nbytes)), dtype=torch.uint8, device=device)
+            return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
-        return cls(rows, K, (p4, p6, p8), buf(p4 // 2), buf(3 * p6 // 4), buf(p8), buf(K // 32))
+        return cls(rows, K, split, buf(sz["q4"]), buf(sz["q6"]), buf(sz["q8"]), buf(sz["sc"]))
 
     def descriptor(self) -> MMTensor:
         d = MMTensor()
         d.rows, d.K = self.rows, self.K
         d.split = MMSplit(*self.split)
-        for name, ld in (("q4", "ld4"), ("q6", "ld6"), ("q8", "ld8"), ("sc", "ldsc")):
+        for name in ("q4", "q6", "q8", "sc"):
             t = getattr(self, name)
             setattr(d, name, t.data_ptr() if t is not None else None)
-            setattr(d, ld, t.stride(0) if t is not None else 0)
         return d
 
-    def host_arrays(self):
-        """Meaningful bytes of each buffer as numpy arrays (for comparisons)."""
+    def raw_host(self) -> dict:
+        """The four buffers' bytes as numpy arrays (empty for an absent group)."""
         import numpy as np
 
-        p4, p6, p8 = self.split
-
-        def get(t, n):
-            if t is None:
-                return np.zeros((self.rows, 0), np.uint8)
-            return t[:, :n].cpu().numpy()
-
-        return {"q4": get(self.q4, p4 // 2), "q6": get(self.q6, 3 * p6 // 4), "q8": get(self.q8, p8),
-                "sc": get(self.sc, self.K // 32)}
+        return {k: (getattr(self, k).cpu().numpy() if getattr(self, k) is not None else np.zeros(0, np.uint8))
+                for k in ("q4", "q6", "q8", "sc")}
 
 
 def _quantize(fn, x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None, stream) -> MXTensor:

@@ -30,36 +30,51 @@ mm_status fail(mm_status s, const char* fmt, ...) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-int64_t round16(int64_t v) { return (v + 15) & ~(int64_t)15; }
+// Layout arithmetic of include/micromix.h.
+struct Layout {
+  int64_t rp;         // rows rounded up to a row group
+  int nb[3];          // blocks per group
+  int steps[3];       // steps per group
+  int64_t bytes[4];   // q4, q6, q8, sc
+};
+
+Layout layout(int64_t rows, mm_split s) {
+  Layout l;
+  l.rp = (rows + mm::kRowGroup - 1) / mm::kRowGroup * mm::kRowGroup;
+  const int p[3] = {s.p4, s.p6, s.p8};
+  int64_t total_steps = 0;
+  for (int g = 0; g < 3; ++g) {
+    l.nb[g] = p[g] / 32;
+    l.steps[g] = (l.nb[g] + mm::kStepBlocks - 1) / mm::kStepBlocks;
+    l.bytes[g] = (int64_t)l.steps[g] * l.rp * mm::step_row_bytes(g);
+    total_steps += l.steps[g];
+  }
+  l.bytes[3] = total_steps * l.rp * mm::kStepBlocks;
+  return l;
+}
+
+mm_status check_shape(int64_t rows, int64_t K, mm_split s, const char* name) {
+  if (rows <= 0 || rows >= kMaxRows) return fail(MM_ERR_SHAPE, "%s: rows=%lld out of range", name, (long long)rows);
+  if (K <= 0 || K % 32 != 0 || K > ((int64_t)1 << 30))
+    return fail(MM_ERR_SHAPE, "%s: K=%lld must be a positive multiple of 32", name, (long long)K);
+  if (s.p4 < 0 || s.p6 < 0 || s.p8 < 0 || s.p4 % 32 || s.p6 % 32 || s.p8 % 32 || (int64_t)s.p4 + s.p6 + s.p8 != K)
+    return fail(MM_ERR_SPLIT, "%s: split (%d,%d,%d) must be non-negative multiples of 32 summing to K=%lld", name,
+                s.p4, s.p6, s.p8, (long long)K);
+  return MM_OK;
+}
 
 // Checks shared by both quantise calls and the GEMM.
 mm_status check_tensor(const mm_mx_tensor* t, const char* name) {
   if (!t) return fail(MM_ERR_NULL, "%s: descriptor is NULL", name);
-  if (t->rows <= 0 || t->rows >= kMaxRows) return fail(MM_ERR_SHAPE, "%s: rows=%lld out of range", name, (long long)t->rows);
-  if (t->K <= 0 || t->K % 32 != 0 || t->K > ((int64_t)1 << 30))
-    return fail(MM_ERR_SHAPE, "%s: K=%lld must be a positive multiple of 32", name, (long long)t->K);
-  const mm_split s = t->split;
-  if (s.p4 < 0 || s.p6 < 0 || s.p8 < 0 || s.p4 % 32 || s.p6 % 32 || s.p8 % 32 ||
-      (int64_t)s.p4 + s.p6 + s.p8 != t->K)
-    return fail(MM_ERR_SPLIT, "%s: split (%d,%d,%d) must be non-negative multiples of 32 summing to K=%lld", name,
-                s.p4, s.p6, s.p8, (long long)t->K);
-  struct {
-    const uint8_t* p;
-    int64_t ld;
-    int64_t need;
-    const char* what;
-  } bufs[4] = {{t->q4, t->ld4, (int64_t)s.p4 / 2, "q4"},
-               {t->q6, t->ld6, (int64_t)s.p6 * 3 / 4, "q6"},
-               {t->q8, t->ld8, (int64_t)s.p8, "q8"},
-               {t->sc, t->ldsc, t->K / 32, "sc"}};
-  for (auto& b : bufs) {
-    if (b.need == 0) continue;
-    if (!b.p) return fail(MM_ERR_NULL, "%s.%s is NULL", name, b.what);
-    if (!aligned16(b.p)) return fail(MM_ERR_ALIGN, "%s.%s is not 16-byte aligned", name, b.what);
-    if (b.ld % 16 != 0) return fail(MM_ERR_ALIGN, "%s.ld of %s=%lld is not a multiple of 16", name, b.what, (long long)b.ld);
-    if (b.ld < round16(b.need))
-      return fail(MM_ERR_SHAPE, "%s.ld of %s=%lld is below %lld", name, b.what, (long long)b.ld,
-                  (long long)round16(b.need));
+  mm_status st = check_shape(t->rows, t->K, t->split, name);
+  if (st != MM_OK) return st;
+  const Layout l = layout(t->rows, t->split);
+  const uint8_t* ptrs[4] = {t->q4, t->q6, t->q8, t->sc};
+  const char* what[4] = {"q4", "q6", "q8", "sc"};
+  for (int b = 0; b < 4; ++b) {
+    if (l.bytes[b] == 0) continue;
+    if (!ptrs[b]) return fail(MM_ERR_NULL, "%s.%s is NULL", name, what[b]);
+    if (!aligned16(ptrs[b])) return fail(MM_ERR_ALIGN, "%s.%s is not 16-byte aligned", name, what[b]);
   }
   return MM_OK;
 }
@@ -75,22 +90,22 @@ mm_status quantize(const void* x, int64_t ldx, const int32_t* perm, const mm_mx_
   if (ldx < out->K) return fail(MM_ERR_SHAPE, "%s: ld=%lld below K=%lld", who, (long long)ldx, (long long)out->K);
   if (!aligned16(x) || ldx % 8 != 0) return fail(MM_ERR_ALIGN, "%s: input must be 16-byte aligned with ld %% 8 == 0", who);
   if (!aligned16(perm)) return fail(MM_ERR_ALIGN, "%s: perm must be 16-byte aligned", who);
+  const Layout l = layout(out->rows, out->split);
   mm::QuantArgs a;
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx;
   a.perm = perm;
   a.rows = out->rows;
+  a.rp = l.rp;
   a.K = (int)out->K;
-  a.nb4 = out->split.p4 / 32;
-  a.nb6 = out->split.p6 / 32;
-  a.q4 = out->q4;
-  a.ld4 = out->ld4;
-  a.q6 = out->q6;
-  a.ld6 = out->ld6;
-  a.q8 = out->q8;
-  a.ld8 = out->ld8;
+  for (int g = 0; g < 3; ++g) {
+    a.nb[g] = l.nb[g];
+    a.steps[g] = l.steps[g];
+  }
+  a.q[0] = out->q4;
+  a.q[1] = out->q6;
+  a.q[2] = out->q8;
   a.sc = out->sc;
-  a.ldsc = out->ldsc;
   hipError_t e = mm::launch_quantize(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "%s: launch failed: %s", who, hipGetErrorString(e));
   return MM_OK;
@@ -101,12 +116,9 @@ mm::Operand operand(const mm_mx_tensor* t) {
   o.q[0] = t->q4;
   o.q[1] = t->q6;
   o.q[2] = t->q8;
-  o.ld[0] = t->ld4;
-  o.ld[1] = t->ld6;
-  o.ld[2] = t->ld8;
   o.sc = t->sc;
-  o.ldsc = t->ldsc;
   o.rows = t->rows;
+  o.rp = layout(t->rows, t->split).rp;
   return o;
 }
 
@@ -139,14 +151,26 @@ mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, in
   mm::GemmArgs g;
   g.w = operand(w);
   g.x = operand(a);
-  g.nb[0] = a->split.p4 / 32;
-  g.nb[1] = a->split.p6 / 32;
-  g.nb[2] = a->split.p8 / 32;
+  const Layout l = layout(a->rows, a->split);
+  for (int k = 0; k < 3; ++k) g.steps[k] = l.steps[k];
   g.y = static_cast<uint16_t*>(y_bf16);
   g.ldy = ldy;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = a->rows <= kDirectMaxM ? mm::launch_gemm_direct(g, s) : mm::launch_gemm_tiled(g, s);
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "mm_gemm: launch failed: %s", hipGetErrorString(e));
+  return MM_OK;
+}
+
+mm_status mm_mx_layout_sizes(int64_t rows, int64_t K, mm_split split, mm_mx_sizes* out) {
+  g_err[0] = 0;
+  if (!out) return fail(MM_ERR_NULL, "mm_mx_layout_sizes: out is NULL");
+  mm_status st = check_shape(rows, K, split, "mm_mx_layout_sizes");
+  if (st != MM_OK) return st;
+  const Layout l = layout(rows, split);
+  out->q4 = l.bytes[0];
+  out->q6 = l.bytes[1];
+  out->q8 = l.bytes[2];
+  out->sc = l.bytes[3];
   return MM_OK;
 }
 

@@ -28,20 +28,9 @@ namespace mm {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-// Operand bytes past a group's last block must read as zero codes, and their
-// scales as 1.0 (E8M0 127).  Loads of such bytes are redirected to these
-// constants instead of being predicated: a predicated load is turned into a
-// branch that waits for the load to finish.
-// (Never written: plain __device__ data so that it lives in the global
-// address space and every operand load stays a global_load.)
-__device__ __attribute__((aligned(16))) uint8_t kZeroCodes[32] = {};
-__device__ uint8_t kScaleOne = 127;
-
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Loads through an explicit global-address-space pointer (a select between a
-// tensor pointer and kZeroCodes would otherwise become a flat load).
 __device__ __forceinline__ uint4 gload16(const void* p) {
   const u32x4 v = *(const __attribute__((address_space(1))) u32x4*)(p);
   return make_uint4(v.x, v.y, v.z, v.w);
@@ -50,34 +39,25 @@ __device__ __forceinline__ uint2 gload8(const void* p) {
   const u32x2 v = *(const __attribute__((address_space(1))) u32x2*)(p);
   return make_uint2(v.x, v.y);
 }
-__device__ __forceinline__ uint32_t gload1(const void* p) {
-  return *(const __attribute__((address_space(1))) uint8_t*)(p);
-}
-
-// Bytes of one 32-element block of a group.
-__host__ __device__ constexpr int block_bytes(int group) { return group == 0 ? 16 : (group == 1 ? 24 : 32); }
 
 // MFMA format selector of a group.
 __host__ __device__ constexpr int group_fmt(int group) { return group == 0 ? kE2M1 : (group == 1 ? kE3M2 : kE4M3); }
 
-// Load the 16 x 128 operand tile fragment of one lane directly from global
-// memory.  `row` is the (already clamped) operand row, `blk0` the first block
-// of this K step inside the group, `nvalid` how many of its 4 blocks exist.
-// Blocks past the group's end contribute exact zeros.
+// One lane's 16 x 128 operand fragment (16 x 16 x 128 form, lane 16 g + r)
+// straight from the packed layout: row n, step `step` of group G.  The padded
+// layout makes every step whole, so there is no bounds logic here.
 template <int G>
-__device__ __forceinline__ v8i load_frag_global(const uint8_t* base, int64_t ld, int64_t row, int blk0, int nvalid,
-                                                int g) {
+__device__ __forceinline__ v8i load_frag16_global(const uint8_t* base, int64_t rp, int64_t n, int64_t step, int g) {
   v8i v;
-  const uint8_t* p = base + row * ld;
   if constexpr (G == 0) {
-    const uint4 d = gload16(g < nvalid ? p + (int64_t)(blk0 + g) * 16 : kZeroCodes);
+    const uint4 d = gload16(base + code_offset<0>(step, rp, n, g));
     v[0] = (int)d.x;
     v[1] = (int)d.y;
     v[2] = (int)d.z;
     v[3] = (int)d.w;
     v[4] = v[5] = v[6] = v[7] = 0;
   } else if constexpr (G == 1) {
-    const uint8_t* s = g < nvalid ? p + (int64_t)(blk0 + g) * 24 : kZeroCodes;
+    const uint8_t* s = base + code_offset<1>(step, rp, n, g);
     const uint2 d0 = gload8(s), d1 = gload8(s + 8), d2 = gload8(s + 16);
     v[0] = (int)d0.x;
     v[1] = (int)d0.y;
@@ -87,9 +67,11 @@ __device__ __forceinline__ v8i load_frag_global(const uint8_t* base, int64_t ld,
     v[5] = (int)d2.y;
     v[6] = v[7] = 0;
   } else {
-    const uint8_t* s = p + (int64_t)blk0 * 32;
-    const uint4 lo = gload16((g >> 1) < nvalid ? s + 16 * g : kZeroCodes);
-    const uint4 hi = gload16(2 + (g >> 1) < nvalid ? s + 64 + 16 * g : kZeroCodes);
+    // channels 16g .. 16g+15: block g/2, half g%2, i.e. record slot g; and
+    // channels 64+16g ..: block 2 + g/2, half g%2, record slot 4 + g
+    const uint8_t* s = base + code_offset<2>(step, rp, n, 0);
+    const uint4 lo = gload16(s + g * 512);
+    const uint4 hi = gload16(s + (4 + g) * 512);
     v[0] = (int)lo.x;
     v[1] = (int)lo.y;
     v[2] = (int)lo.z;
@@ -102,9 +84,9 @@ __device__ __forceinline__ v8i load_frag_global(const uint8_t* base, int64_t ld,
   return v;
 }
 
-// E8M0 scale of block `blk` of a row, or 1.0 past the group's end.
-__device__ __forceinline__ int load_scale(const uint8_t* row_sc, int blk, bool valid) {
-  return gload1(valid ? row_sc + blk : &kScaleOne);
+// E8M0 scale of block j of global step t of row n.
+__device__ __forceinline__ int load_scale(const uint8_t* sc, int64_t rp, int64_t t, int64_t n, int j) {
+  return *(const __attribute__((address_space(1))) uint8_t*)(sc + (t * rp + n) * kStepBlocks + j);
 }
 
 // acc = acc + A(group G) x B(group G) with per-block E8M0 scales sa / sb.

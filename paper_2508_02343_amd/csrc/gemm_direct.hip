@@ -13,31 +13,27 @@ constexpr int kDirectWaves = 4;
 template <int TN, int TM, int G>
 __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][TM], int64_t n0, int64_t m0,
                                              int wave, int lane) {
-  const int nb = a.nb[G];
-  if (nb == 0) return;
+  const int S = a.steps[G];
+  if (S == 0) return;
   const int g = lane >> 4, r = lane & 15;
-  int gblk0 = 0;  // first block of this group inside the scale rows
-  if (G >= 1) gblk0 += a.nb[0];
-  if (G >= 2) gblk0 += a.nb[1];
-  const int nsteps = (nb + 3) >> 2;
-  for (int ks = wave; ks < nsteps; ks += kDirectWaves) {
-    const int blk0 = ks * 4;
-    const int nvalid = nb - blk0 < 4 ? nb - blk0 : 4;
+  // global step index of this group's first step inside the scale buffer
+  const int t0 = (G >= 1 ? a.steps[0] : 0) + (G >= 2 ? a.steps[1] : 0);
+  for (int s = wave; s < S; s += kDirectWaves) {
     v8i wf[TN], xf[TM];
     int ws[TN], xs[TM];
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
       int64_t n = n0 + 16 * i + r;
-      n = n < a.w.rows ? n : a.w.rows - 1;
-      wf[i] = load_frag_global<G>(a.w.q[G], a.w.ld[G], n, blk0, nvalid, g);
-      ws[i] = load_scale(a.w.sc + n * a.w.ldsc, gblk0 + blk0 + g, g < nvalid);
+      n = n < a.w.rp ? n : a.w.rp - 1;  // padded rows exist up to rp
+      wf[i] = load_frag16_global<G>(a.w.q[G], a.w.rp, n, s, g);
+      ws[i] = load_scale(a.w.sc, a.w.rp, t0 + s, n, g);
     }
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       int64_t m = m0 + 16 * j + r;
-      m = m < a.x.rows ? m : a.x.rows - 1;
-      xf[j] = load_frag_global<G>(a.x.q[G], a.x.ld[G], m, blk0, nvalid, g);
-      xs[j] = load_scale(a.x.sc + m * a.x.ldsc, gblk0 + blk0 + g, g < nvalid);
+      m = m < a.x.rp ? m : a.x.rp - 1;
+      xf[j] = load_frag16_global<G>(a.x.q[G], a.x.rp, m, s, g);
+      xs[j] = load_scale(a.x.sc, a.x.rp, t0 + s, m, g);
     }
 #pragma unroll
     for (int i = 0; i < TN; ++i)

@@ -6,37 +6,53 @@
 
 namespace mm {
 
+// Packed-layout constants (the layout is documented in include/micromix.h).
+constexpr int kRowGroup = 32;   // rows per row group
+constexpr int kStepBlocks = 4;  // blocks per step
+// Bytes of one row's step per group: E2M1, E3M2, E4M3.
+__host__ __device__ constexpr int step_row_bytes(int group) { return group == 0 ? 64 : (group == 1 ? 96 : 128); }
+// Bytes of one 32-element block per group.
+__host__ __device__ constexpr int block_bytes(int group) { return group == 0 ? 16 : (group == 1 ? 24 : 32); }
+
+// Byte offset, inside a group's code buffer, of block j (0..3) of step `step`
+// of row n (row-group record, block-major): E2M1 16 bytes, E3M2 24 bytes,
+// E4M3 the first 16 bytes (the second 16 are 512 bytes further on).
+template <int G>
+__host__ __device__ __forceinline__ int64_t code_offset(int64_t step, int64_t rp, int64_t n, int j) {
+  constexpr int RB = step_row_bytes(G);
+  const int64_t rec = (step * rp + (n & ~(int64_t)(kRowGroup - 1))) * RB;
+  const int r = (int)(n & (kRowGroup - 1));
+  if constexpr (G == 0) return rec + j * 512 + r * 16;
+  else if constexpr (G == 1) return rec + j * 768 + r * 24;
+  else return rec + (2 * j) * 512 + r * 16;
+}
+
 // Fused reorder-and-quantize of `rows` bf16 rows (activations or weights).
 struct QuantArgs {
   const uint16_t* x;
   int64_t ldx;  // elements
   const int32_t* perm;
   int64_t rows;
+  int64_t rp;    // rows rounded up to a row group
   int K;
-  int nb4, nb6;  // block counts of the E2M1 and E3M2 groups
-  uint8_t* q4;
-  int64_t ld4;
-  uint8_t* q6;
-  int64_t ld6;
-  uint8_t* q8;
-  int64_t ld8;
+  int nb[3];     // blocks per group
+  int steps[3];  // steps per group
+  uint8_t* q[3];
   uint8_t* sc;
-  int64_t ldsc;
 };
 
 // One quantised GEMM operand.
 struct Operand {
   const uint8_t* q[3];  // E2M1, E3M2, E4M3 code buffers
-  int64_t ld[3];
   const uint8_t* sc;
-  int64_t ldsc;
   int64_t rows;
+  int64_t rp;  // rows rounded up to a row group
 };
 
 struct GemmArgs {
-  Operand w;  // first MFMA operand: weight rows (output columns n)
-  Operand x;  // second MFMA operand: activation rows (output rows m)
-  int nb[3];  // blocks per group
+  Operand w;     // first MFMA operand: weight rows (output columns n)
+  Operand x;     // second MFMA operand: activation rows (output rows m)
+  int steps[3];  // steps per group
   uint16_t* y;
   int64_t ldy;
 };

@@ -5,10 +5,11 @@
 //
 // HBM-bound design for gfx950:
 //  - a pass is `rpp` consecutive rows; the grid is sized to the number of
-//    workgroups the chip holds at once and workgroup g takes passes g,
-//    g + grid, ...; one thread per (row, 32-channel block), so each thread
-//    always quantises the same block index and keeps that block's 32 sigma
-//    entries in registers, as LDS byte addresses, for the whole workgroup;
+//    workgroups the chip holds at once, each XCD takes a contiguous range of
+//    passes and its workgroups stride through it; one thread per (row,
+//    32-channel block), so each thread always quantises the same block index
+//    and keeps that block's 32 sigma entries in registers, as LDS byte
+//    addresses, for the whole workgroup;
 //  - rows arrive with 16-byte coalesced loads (the only HBM read) into
 //    registers and are written to one of two LDS stages: the loads of pass
 //    p+1 are in flight while pass p is quantised from the other stage;
@@ -57,18 +58,42 @@ __device__ __forceinline__ uint32_t min_u16x2(uint32_t a, uint32_t b) {
                             __builtin_elementwise_min(__builtin_bit_cast(u16x2, a), __builtin_bit_cast(u16x2, b)));
 }
 
-// Quantise one 32-channel block of one row from LDS stage kStage.
+// Zero codes and scale byte for block j of step `step` of row n (padding).
+template <int G>
+__device__ __forceinline__ void zero_block(const QuantArgs& a, int64_t step, int64_t gstep, int64_t n, int j) {
+  uint8_t* dst = a.q[G] + code_offset<G>(step, a.rp, n, j);
+  if constexpr (G == 0) {
+    *reinterpret_cast<uint4*>(dst) = make_uint4(0u, 0u, 0u, 0u);
+  } else if constexpr (G == 1) {
+    uint2* d = reinterpret_cast<uint2*>(dst);
+    d[0] = d[1] = d[2] = make_uint2(0u, 0u);
+  } else {
+    *reinterpret_cast<uint4*>(dst) = make_uint4(0u, 0u, 0u, 0u);
+    *reinterpret_cast<uint4*>(dst + 512) = make_uint4(0u, 0u, 0u, 0u);
+  }
+  a.sc[(gstep * a.rp + n) * kStepBlocks + j] = 0;
+}
+
+template <int G>
+__device__ __forceinline__ void zero_tail(const QuantArgs& a, int64_t step, int64_t gstep, int64_t n, int j) {
+  for (int jj = j + 1; jj < kStepBlocks; ++jj) zero_block<G>(a, step, gstep, n, jj);
+}
+
+// Quantise block b (local to its group) of row n from LDS stage kStage; rows
+// past a.rows are padding and quantise an all-zero block.  The thread that
+// owns a group's last block also zeroes the padding blocks of that step.
 template <int kStage>
-__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, const QuantArgs& a,
-                                               int64_t row, int blk) {
+__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, const QuantArgs& a, int64_t n,
+                                               int b, int gstep0) {
   // gather: the block's 32 permuted channels as 16 packed bf16 pairs
   uint32_t d[16];
+  const bool pad_row = n >= a.rows;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     u16x2 v;
     v.x = lds_u16(addr[2 * i] + kStage * kStageOff);
     v.y = lds_u16(addr[2 * i + 1] + kStage * kStageOff);
-    d[i] = __builtin_bit_cast(uint32_t, v);
+    d[i] = pad_row ? 0u : __builtin_bit_cast(uint32_t, v);
   }
 
   // absmax: bf16 magnitudes compare as unsigned integers
@@ -90,6 +115,10 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
   // the conversions read the scale's E8M0 exponent from an fp32 operand
   const float scale = __uint_as_float(sbyte << 23);
 
+  const int64_t step = b >> 2;
+  const int j = b & 3;
+  const int64_t gstep = gstep0 + step;
+  const bool last = b == a.nb[group] - 1;
   if (group == 0) {
     uint32_t w[4];
 #pragma unroll
@@ -101,21 +130,18 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
       v = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(v, __builtin_bit_cast(bf16x2, d[4 * q + 3]), scale, 3);
       w[q] = v;
     }
-    *reinterpret_cast<uint4*>(a.q4 + row * a.ld4 + (int64_t)blk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4*>(a.q[0] + code_offset<0>(step, a.rp, n, j)) = make_uint4(w[0], w[1], w[2], w[3]);
+    if (last) zero_tail<0>(a, step, gstep, n, j);
   } else if (group == 1) {
     u32x16 v;
 #pragma unroll
     for (int i = 0; i < 16; ++i) v[i] = d[i];
     const i32x6 c = __builtin_amdgcn_cvt_scalef32_pk32_bf6_bf16(__builtin_bit_cast(bf16x32, v), scale);
-    const int b6 = blk - a.nb4;
-    uint2* dst = reinterpret_cast<uint2*>(a.q6 + row * a.ld6 + (int64_t)b6 * 24);
+    uint2* dst = reinterpret_cast<uint2*>(a.q[1] + code_offset<1>(step, a.rp, n, j));
     dst[0] = make_uint2((uint32_t)c[0], (uint32_t)c[1]);
     dst[1] = make_uint2((uint32_t)c[2], (uint32_t)c[3]);
     dst[2] = make_uint2((uint32_t)c[4], (uint32_t)c[5]);
-    // An odd number of E3M2 blocks ends the row 8 bytes short of a 16-byte
-    // boundary; those padding bytes are part of the layout and read as zero
-    // codes by the GEMM's 16-byte loads.
-    if (b6 == a.nb6 - 1 && (a.nb6 & 1)) dst[3] = make_uint2(0u, 0u);
+    if (last) zero_tail<1>(a, step, gstep, n, j);
   } else {
     // 448 * 2^e in bf16: biased exponent e + 127 + 8 = sbyte + 8, mantissa 0x60
     const uint32_t lim = ((sbyte + 8u) << 7) | 0x60u;
@@ -123,7 +149,7 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
     uint32_t w[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      // clamp the magnitudes, keep the signs (bitfield insert)
+      // clamp the magnitudes, keep the signs
       const uint32_t c0 = min_u16x2(d[2 * q] & 0x7FFF7FFFu, lim2) | (d[2 * q] & 0x80008000u);
       const uint32_t c1 = min_u16x2(d[2 * q + 1] & 0x7FFF7FFFu, lim2) | (d[2 * q + 1] & 0x80008000u);
       i16x2 v = {0, 0};
@@ -131,11 +157,12 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
       v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c1), scale, true);
       w[q] = __builtin_bit_cast(uint32_t, v);
     }
-    uint4* dst = reinterpret_cast<uint4*>(a.q8 + row * a.ld8 + (int64_t)(blk - a.nb4 - a.nb6) * 32);
-    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
-    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    uint8_t* dst = a.q[2] + code_offset<2>(step, a.rp, n, j);
+    *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4*>(dst + 512) = make_uint4(w[4], w[5], w[6], w[7]);
+    if (last) zero_tail<2>(a, step, gstep, n, j);
   }
-  a.sc[row * a.ldsc + blk] = (uint8_t)sbyte;
+  a.sc[(gstep * a.rp + n) * kStepBlocks + j] = (uint8_t)sbyte;
 }
 
 }  // namespace
@@ -157,8 +184,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   const bool active = prow < rpp;
   const int stage_bytes = rpp * K * 2;
   const int nchunks = stage_bytes >> 4;  // 16-byte chunks per pass
-  const int64_t passes = (a.rows + rpp - 1) / rpp;
-  const int64_t stride = gridDim.x;
+  const int64_t passes = (a.rp + rpp - 1) / rpp;  // padding rows included
 
   // sigma of this thread's block as LDS byte addresses within a stage; an
   // out-of-range entry (a caller error) is clamped to stay inside the row
@@ -175,7 +201,9 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   // factored out and re-added before every LDS read
 #pragma unroll
   for (int i = 0; i < 32; ++i) asm volatile("" : "+v"(addr[i]));
-  const int group = blk < a.nb4 ? 0 : (blk < a.nb4 + a.nb6 ? 1 : 2);
+  const int group = blk < a.nb[0] ? 0 : (blk < a.nb[0] + a.nb[1] ? 1 : 2);
+  const int b = blk - (group >= 1 ? a.nb[0] : 0) - (group >= 2 ? a.nb[1] : 0);  // block within its group
+  const int gstep0 = (group >= 1 ? a.steps[0] : 0) + (group >= 2 ? a.steps[1] : 0);
 
   // 16-byte chunk c of a pass lies in pass-row c / (K/8); rows past the end
   // are read from the last row (their results are never stored) and chunks
@@ -205,19 +233,32 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
     }                                                                                                \
   }
 
-  int64_t q = blockIdx.x;
+  // Workgroups are dealt to the 8 XCDs round-robin; each XCD takes a
+  // contiguous range of passes, so the rows of one 32-row group (which share
+  // cache lines in the packed layout) are written through one XCD's L2.
+  int64_t q, q_end, stride;
+  if (gridDim.x % 8 == 0) {
+    const int x = blockIdx.x & 7;
+    q = passes * x / 8 + (blockIdx.x >> 3);
+    q_end = passes * (x + 1) / 8;
+    stride = gridDim.x / 8;
+  } else {
+    q = blockIdx.x;
+    q_end = passes;
+    stride = gridDim.x;
+  }
   MM_LOAD_PASS(q);
   MM_STORE_PASS(0);
   __syncthreads();
-  for (int i = 0; q < passes; ++i, q += stride) {
-    const bool more = kPipe && q + stride < passes;
+  for (int i = 0; q < q_end; ++i, q += stride) {
+    const bool more = kPipe && q + stride < q_end;
     if (more) MM_LOAD_PASS(q + stride);
     const int64_t row = q * rpp + prow;
-    if (active && row < a.rows) {
+    if (active && row < a.rp) {
       if ((i & 1) == 0)
-        quantize_block<0>(addr, group, a, row, blk);
+        quantize_block<0>(addr, group, a, row, b, gstep0);
       else
-        quantize_block<1>(addr, group, a, row, blk);
+        quantize_block<1>(addr, group, a, row, b, gstep0);
     }
     if (more) MM_STORE_PASS((i + 1) & 1);
     __syncthreads();
@@ -272,7 +313,7 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
     const size_t lds = (size_t)K * 2 + 16;
     hipError_t e = allow_lds<1024, false>(lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((quantize_rows_kernel<1024, false>), dim3((unsigned)a.rows), dim3(T), lds, stream, a, 1);
+    hipLaunchKernelGGL((quantize_rows_kernel<1024, false>), dim3((unsigned)a.rp), dim3(T), lds, stream, a, 1);
     return hipGetLastError();
   }
   // rows per pass: the fewest idle lanes (ties: more rows) among launches of
@@ -291,7 +332,7 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
     if (t >= 256) break;
   }
   const int T = (rpp * nblk + 63) / 64 * 64;
-  const int64_t passes = (a.rows + rpp - 1) / rpp;
+  const int64_t passes = (a.rp + rpp - 1) / rpp;
   // two stages plus the 16-byte dummy slot
   const size_t lds = (size_t)kStageOff + (size_t)rpp * K * 2 + 16;
   hipError_t e = allow_lds<512, true>(lds);

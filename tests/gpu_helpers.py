@@ -9,6 +9,7 @@ import numpy as np
 import torch
 
 from oracle import mx_oracle as O
+from tests import packed_layout as L
 
 
 def note(msg: str) -> None:
@@ -26,17 +27,37 @@ def to_dev_perm(perm: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(perm, dtype=np.int32)).cuda()
 
 
-def assert_codes_equal(gpu: dict, ref: O.MXTensor, rows=None, ctx: str = "") -> None:
-    """Byte-exact comparison of q4/q6/q8/sc (optionally of selected rows)."""
+def _first_diff(g, r, ctx, name):
+    bad = np.argwhere(g != r)
+    idx = tuple(bad[0])
+    raise AssertionError(f"{ctx} {name}: {len(bad)} bytes differ; first at {idx}: "
+                         f"gpu {g[idx]:#04x} oracle {r[idx]:#04x}")
+
+
+def assert_codes_equal(t, ref: O.MXTensor, rows=None, ctx: str = "") -> None:
+    """Byte-exact comparison of a binding MXTensor's buffers with the oracle.
+
+    rows=None: ref covers all rows; every byte of the four packed buffers,
+    padding included, must equal the oracle's codes and scales laid out per
+    the header.  Otherwise ref covers only the listed rows, which are
+    compared after unpacking the GPU's buffers to row-major form.
+    """
+    raw = t.raw_host()
+    if rows is None:
+        want = L.tile(ref.q4, ref.q6, ref.q8, ref.sc, t.rows, t.split)
+        for name in ("q4", "q6", "q8", "sc"):
+            g, r = raw[name], want[name]
+            assert g.shape == r.shape, (ctx, name, g.shape, r.shape)
+            if not np.array_equal(g, r):
+                _first_diff(g, r, ctx, name)
+        return
+    got = L.untile(raw, t.rows, t.split)
     for name in ("q4", "q6", "q8", "sc"):
-        g = gpu[name] if rows is None else gpu[name][rows]
+        g = got[name][rows]
         r = np.asarray(getattr(ref, name))
         assert g.shape == r.shape, (ctx, name, g.shape, r.shape)
         if not np.array_equal(g, r):
-            bad = np.argwhere(g != r)
-            i, j = bad[0]
-            raise AssertionError(f"{ctx} {name}: {len(bad)} bytes differ; first at row {i} byte {j}: "
-                                 f"gpu {g[i, j]:#04x} oracle {r[i, j]:#04x}")
+            _first_diff(g, r, ctx, name)
 
 
 def y_to_f64(y: torch.Tensor) -> np.ndarray:

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(b.LIB_PATH)
     for n in _declared_functions():
         assert hasattr(lib, n), n
-    assert b.lib.mm_abi_version() == 1
+    assert b.lib.mm_abi_version() == 2
 
 
 def test_status_strings():
@@ -45,17 +45,13 @@ def test_status_strings():
 FAKE = 0x10000  # 16-byte aligned, never dereferenced: validation fails first
 
 
-def _tensor(rows=4, K=128, split=(64, 32, 32), ld=None, ptr=FAKE):
+def _tensor(rows=4, K=128, split=(64, 32, 32), ptr=FAKE):
     d = b.MMTensor()
     d.rows, d.K = rows, K
     d.split = b.MMSplit(*split)
-    p4, p6, p8 = split
-    need = {"4": p4 // 2, "6": 3 * p6 // 4, "8": p8, "sc": K // 32}
-    for key, nb in need.items():
-        name = "q" + key if key != "sc" else "sc"
-        ldname = "ld" + key if key != "sc" else "ldsc"
-        setattr(d, name, ptr if nb else None)
-        setattr(d, ldname, ld if ld is not None else (nb + 15) // 16 * 16)
+    for name, p in zip(("q4", "q6", "q8"), split):
+        setattr(d, name, ptr if p else None)
+    d.sc = ptr
     return d
 
 
@@ -75,8 +71,7 @@ def _q(d, x=FAKE, ldx=None, perm=FAKE):
         (lambda d: setattr(d, "q4", None), "MM_ERR_NULL"),
         (lambda d: setattr(d, "sc", None), "MM_ERR_NULL"),
         (lambda d: setattr(d, "q6", FAKE + 8), "MM_ERR_ALIGN"),
-        (lambda d: setattr(d, "ld8", 24), "MM_ERR_ALIGN"),
-        (lambda d: setattr(d, "ld4", 16), "MM_ERR_SHAPE"),
+        (lambda d: setattr(d, "sc", FAKE + 4), "MM_ERR_ALIGN"),
     ],
 )
 def test_quantize_rejects_bad_descriptors(mutate, expect):
@@ -103,7 +98,7 @@ def test_quantize_rejects_bad_inputs():
 def test_empty_groups_may_be_null_but_rest_is_checked():
     d = _tensor(split=(128, 0, 0))
     assert d.q6 is None and d.q8 is None
-    d.ld4 = 8  # too small and misaligned: proves validation still runs
+    d.q4 = FAKE + 8  # misaligned: proves validation still runs
     assert b.STATUS_NAMES[_q(d)] == "MM_ERR_ALIGN"
 
 
@@ -126,11 +121,33 @@ def test_gemm_rejects_mismatched_operands():
     assert b.STATUS_NAMES[_g(bad, w)] == "MM_ERR_SPLIT"
 
 
+@pytest.mark.parametrize("rows,K,split,want", [
+    # rows padded to 32; steps of 4 blocks: E2M1 3 blocks -> 1 step, E3M2 5 -> 2, E4M3 3 -> 1
+    (5, 352, (96, 160, 96), {"q4": 1 * 32 * 64, "q6": 2 * 32 * 96, "q8": 1 * 32 * 128, "sc": 4 * 32 * 4}),
+    (33, 4096, (3072, 768, 256), {"q4": 24 * 64 * 64, "q6": 6 * 64 * 96, "q8": 2 * 64 * 128, "sc": 32 * 64 * 4}),
+    (64, 64, (64, 0, 0), {"q4": 64 * 64, "q6": 0, "q8": 0, "sc": 64 * 4}),
+])
+def test_layout_sizes(rows, K, split, want):
+    assert b.layout_sizes(rows, K, split) == want
+    from tests import packed_layout as L
+
+    assert L.geometry(rows, split)["bytes"] == [want[k] for k in ("q4", "q6", "q8", "sc")]
+
+
+def test_layout_sizes_rejects_bad_shapes():
+    with pytest.raises(b.MMError):
+        b.layout_sizes(4, 96, (64, 16, 16))
+    with pytest.raises(b.MMError):
+        b.layout_sizes(0, 64, (64, 0, 0))
+    assert b.lib.mm_mx_layout_sizes(4, 64, b.MMSplit(64, 0, 0), None) == 1
+
+
 def test_binding_descriptor_fields():
     t = b.MXTensor.empty(5, 352, (96, 160, 96), device="cpu")
     d = t.descriptor()
     assert (d.rows, d.K, d.split.p4, d.split.p6, d.split.p8) == (5, 352, 96, 160, 96)
-    assert (d.ld4, d.ld6, d.ld8, d.ldsc) == (48, 128, 96, 16)
-    assert d.q4 == t.q4.data_ptr() and d.sc == t.sc.data_ptr()
+    assert d.q4 == t.q4.data_ptr() and d.q6 == t.q6.data_ptr() and d.q8 == t.q8.data_ptr()
+    assert d.sc == t.sc.data_ptr()
+    assert t.q4.numel() == 2048 and t.sc.numel() == 512
     e = b.MXTensor.empty(3, 64, (64, 0, 0), device="cpu").descriptor()
-    assert e.q6 is None and e.q8 is None and e.ld6 == 0
+    assert e.q6 is None and e.q8 is None

@@ -37,8 +37,8 @@ def _check_full(xb, wb, perm, split, ctx):
     y = _b().gemm(a, w)
     torch.cuda.synchronize()
     ra, rw = O.quantize_mixed(xb, perm, split), O.quantize_mixed(wb, perm, split)
-    assert_codes_equal(a.host_arrays(), ra, ctx=ctx + " A")
-    assert_codes_equal(w.host_arrays(), rw, ctx=ctx + " W")
+    assert_codes_equal(a, ra, ctx=ctx + " A")
+    assert_codes_equal(w, rw, ctx=ctx + " W")
     assert_gemm_close(y_to_f64(y), O.gemm_mixed(ra, rw), ctx=ctx)
 
 
@@ -79,7 +79,7 @@ def test_decode_configs(w):
     torch.cuda.synchronize()
     cols = np.unique(np.concatenate([[0, w.N - 1], np.random.default_rng(2).choice(w.N, 254, replace=False)]))
     ra, rw = O.quantize_mixed(xb, perm, w.split), O.quantize_mixed(wb[cols], perm, w.split)
-    assert_codes_equal(wq.host_arrays(), rw, rows=cols, ctx=w.name + " W")
+    assert_codes_equal(wq, rw, rows=cols, ctx=w.name + " W")
     assert_gemm_close(y_to_f64(y)[:, cols], O.gemm_mixed(ra, rw), ctx=w.name)
 
 

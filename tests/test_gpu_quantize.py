@@ -31,7 +31,7 @@ def _run(bits, perm, split, weight=False, ld_extra=0):
     fn = b.quantize_weight if weight else b.quantize_act
     out = fn(x, to_dev_perm(perm), split)
     torch.cuda.synchronize()
-    return out.host_arrays()
+    return out
 
 
 def test_tiny_config_activation_and_weight():
@@ -106,7 +106,7 @@ def test_repeatable_bytes():
     w = W.TINY
     note("determinism")
     xb, perm = w.x_bits(), w.perm()
-    a, b = _run(xb, perm, w.split), _run(xb, perm, w.split)
+    a, b = _run(xb, perm, w.split).raw_host(), _run(xb, perm, w.split).raw_host()
     for k in a:
         assert np.array_equal(a[k], b[k])
 
@@ -135,20 +135,21 @@ def test_full_size_weight_sampled_rows():
     assert_codes_equal(got, O.quantize_mixed(wb[rows], perm, w.split), rows=rows, ctx=w.name + " W")
 
 
-@pytest.mark.parametrize("p6", [32, 96, 160])
-def test_e3m2_row_padding_is_zero(p6):
-    """With an odd number of E3M2 blocks the 8 bytes after the last block are
-    written as zeros (part of the packed layout the GEMM reads)."""
-    split = (64, p6, 32)
+@pytest.mark.parametrize("rows,split", [(9, (64, 32, 32)), (40, (32, 96, 160)), (1, (96, 0, 64))])
+def test_padding_is_written_as_zero(rows, split):
+    """Blocks past a group's end inside its last step, and rows past `rows`
+    up to the next multiple of 32, are zero codes and zero scale bytes, even
+    over buffers that held garbage (the GEMM reads them)."""
     K = sum(split)
-    note(f"E3M2 padding p6={p6}")
-    rng = np.random.default_rng(p6)
-    bits = W.f32_to_bf16_bits(rng.standard_normal((9, K)).astype(np.float32))
+    note(f"padding rows={rows} split={split}")
+    rng = np.random.default_rng(rows + K)
+    bits = W.f32_to_bf16_bits(rng.standard_normal((rows, K)).astype(np.float32))
+    perm = rng.permutation(K).astype(np.int32)
     b = _b()
-    out = b.MXTensor.empty(9, K, split)
-    out.q6.fill_(0xAB)
-    b.quantize_act(to_dev_bf16(bits), to_dev_perm(np.arange(K, dtype=np.int32)), split, out=out)
+    out = b.MXTensor.empty(rows, K, split)
+    for t in (out.q4, out.q6, out.q8, out.sc):
+        if t is not None:
+            t.fill_(0xAB)
+    b.quantize_act(to_dev_bf16(bits), to_dev_perm(perm), split, out=out)
     torch.cuda.synchronize()
-    q6 = out.q6.cpu().numpy()
-    n = 3 * p6 // 4
-    assert np.all(q6[:, n:n + 8] == 0)
+    assert_codes_equal(out, O.quantize_mixed(bits, perm, split), ctx="padding")
