@@ -28,8 +28,20 @@ namespace mm {
 
 namespace tiled {
 
-constexpr int kThreads = 256;
 constexpr int kLdsBytes = 160 * 1024;
+
+// Wavefronts per workgroup, in a 2 x (NW/2) grid: 256 x 256 tiles use eight
+// (two per SIMD: while one waits at a barrier or for LDS, the other's MFMAs
+// run; each holds 128 x 64 outputs, 128 accumulator registers), 256 x 128
+// tiles use four (128 x 64 each).
+__host__ __device__ constexpr int tile_waves(int BN, int BM) { return BN * BM >= 256 * 256 ? 8 : 4; }
+template <int BN, int BM>
+struct Shape {
+  static constexpr int NW = tile_waves(BN, BM);
+  static constexpr int kThreads = 64 * NW;
+  static constexpr int WN = BN / 2, WM = BM / (NW / 2);  // wavefront tile
+  static constexpr int TN = WN / 32, TM = WM / 32;       // 32-row fragments per wavefront
+};
 
 // Pipeline plan of group G for a BN x BM tile: a "sub-step" is a whole layout
 // step (four blocks, two 64-channel slices), or half of one where a whole
@@ -47,9 +59,10 @@ struct Plan {
   static constexpr int kStageBytes = kCodeBytes + kRows * kStepBlocks;  // + the step's scale words
   static constexpr int kStages = kLdsBytes / kStageBytes > 8 ? 8 : kLdsBytes / kStageBytes;
   static constexpr int kWInstr = kWBytes / 1024;            // DMA instructions carrying weight codes
-  static constexpr int kCodeLoads = kCodeBytes / 1024 / 4;  // per wavefront
+  static constexpr int NW = Shape<BN, BM>::NW;
+  static constexpr int kCodeLoads = kCodeBytes / 1024 / NW;  // per wavefront
   static constexpr int kLoads = kCodeLoads + 1;             // + the scale words
-  static_assert(kCodeBytes % 4096 == 0 && kWBytes % 1024 == 0, "DMA instructions must split evenly");
+  static_assert(kCodeBytes % (1024 * NW) == 0 && kWBytes % 1024 == 0, "DMA instructions must split evenly");
   static_assert(kStages >= 3, "ring of at least three stages");
   static_assert((kStages - 2) * kLoads < 64, "vmcnt range");
 };
@@ -125,16 +138,18 @@ __device__ __forceinline__ Dma<G, BN, BM> make_dma(const GemmArgs& a, int64_t n0
     grp = grp < last ? grp : last;
     d.off[k] = (uint32_t)(grp * kRowGroup * P::RB + within);
   }
-  // scale words: waves 0-1 the weight rows, waves 2-3 the activation rows,
-  // 4 rows (16 bytes) per lane; rows past the padded rows re-read the last 4
-  const bool op = wave >= 2;
-  const int half = op ? BM / 2 : BN / 2;
+  // scale words: the first half of the wavefronts the weight rows, the
+  // second half the activation rows, 4 rows (16 bytes) per lane; rows past
+  // the padded rows re-read the last 4
+  constexpr int H = P::NW / 2;
+  const bool op = wave >= H;
+  const int per = op ? BM / H : BN / H;  // rows per wavefront
   const int64_t rp = op ? a.x.rp : a.w.rp;
   const int64_t r0 = op ? m0 : n0;
-  int row = (wave & 1) * half + lane * 4;  // row within the tile
+  int row = (wave % H) * per + lane * 4;  // row within the tile
   row = r0 + row + 4 <= rp ? row : (int)(rp - 4 - r0);
   d.soff = (uint32_t)row * kStepBlocks;
-  d.sdst = (uint32_t)(P::kCodeBytes + (op ? BN * kStepBlocks : 0) + (wave & 1) * half * kStepBlocks);
+  d.sdst = (uint32_t)(P::kCodeBytes + (op ? BN * kStepBlocks : 0) + (wave % H) * per * kStepBlocks);
   d.sc[0] = a.w.sc + n0 * kStepBlocks;
   d.sc[1] = a.x.sc + m0 * kStepBlocks;
   return d;
@@ -153,10 +168,11 @@ __device__ __forceinline__ void issue(const Dma<G, BN, BM>& d, uint32_t st, int 
     const int inst = wave * P::kCodeLoads + k;
     dma16_s(d.off[k], inst >= P::kWInstr ? cx : cw, st + inst * 1024);
   }
-  const bool op = wave >= 2;
+  constexpr int H = P::NW / 2;
+  const bool op = wave >= H;
   const int64_t t = d.t0 + s;
   const uint8_t* sb = op ? d.sc[1] + t * d.rp[1] * kStepBlocks : d.sc[0] + t * d.rp[0] * kStepBlocks;
-  if (lane < (op ? BM : BN) / 8) dma16_s(d.soff, sb, st + d.sdst);
+  if (lane < (op ? BM : BN) / H / 4) dma16_s(d.soff, sb, st + d.sdst);
 }
 
 // This lane's 32 x 64 fragment at LDS byte address p (block-major record):
@@ -196,7 +212,7 @@ __device__ __forceinline__ v8i read_frag(uint32_t p) {
 }
 
 template <int BN, int BM>
-using Acc = v16f[BN / 64][BM / 64];
+using Acc = v16f[Shape<BN, BM>::TN][Shape<BN, BM>::TM];
 
 // The MFMAs of one sub-step held in the stage at st (layout-step half u).
 // All activation fragments of the sub-step are read first; weight fragments
@@ -205,7 +221,7 @@ using Acc = v16f[BN / 64][BM / 64];
 template <int G, int BN, int BM>
 __device__ __forceinline__ void compute_step(uint32_t st, int u, int wn0, int wm0, Acc<BN, BM>& acc) {
   using P = Plan<G, BN, BM>;
-  constexpr int TN = BN / 64, TM = BM / 64, SL = P::kSlices;
+  constexpr int TN = Shape<BN, BM>::TN, TM = Shape<BN, BM>::TM, SL = P::kSlices;
   constexpr int kSliceOff = G == 0 ? 1024 : (G == 1 ? 1536 : 2048);  // slice 1 starts two blocks on
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5, r = lane & 31;
@@ -280,7 +296,8 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
 using namespace tiled;
 
 template <int BN, int BM>
-__global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int tiles_n, int tiles_m) {
+__global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(GemmArgs a, int tiles_n, int tiles_m) {
+  using SH = Shape<BN, BM>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
   constexpr int kGroupN = 4;  // weight tiles that share an XCD's L2 at a time
 
@@ -300,15 +317,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int
   const int64_t n0 = (int64_t)tn * BN, m0 = (int64_t)tm * BM;
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: keeps DMA setup scalar
-  const int wn0 = (wave & 1) * (BN / 2);
-  const int wm0 = (wave >> 1) * (BM / 2);
+  const int wn0 = (wave & 1) * SH::WN;
+  const int wm0 = (wave >> 1) * SH::WM;
   const uint32_t lds0 = lds_addr(lds);
 
   Acc<BN, BM> acc;
 #pragma unroll
-  for (int i = 0; i < BN / 64; ++i)
+  for (int i = 0; i < SH::TN; ++i)
 #pragma unroll
-    for (int j = 0; j < BM / 64; ++j)
+    for (int j = 0; j < SH::TM; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
@@ -321,9 +338,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5, r = lane & 31;
 #pragma unroll
-  for (int i = 0; i < BN / 64; ++i)
+  for (int i = 0; i < SH::TN; ++i)
 #pragma unroll
-    for (int j = 0; j < BM / 64; ++j)
+    for (int j = 0; j < SH::TM; ++j)
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
         const v4f c = {acc[i][j][4 * h], acc[i][j][4 * h + 1], acc[i][j][4 * h + 2], acc[i][j][4 * h + 3]};
@@ -341,7 +358,7 @@ static hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
     attr_set = true;
   }
   const int tn = (int)((a.w.rows + BN - 1) / BN), tm = (int)((a.x.rows + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM>), dim3((unsigned)(tn * tm)), dim3(kThreads), kLdsBytes, stream, a,
+  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads), kLdsBytes, stream, a,
                      tn, tm);
   return hipGetLastError();
 }
