@@ -252,6 +252,10 @@ __device__ __forceinline__ void compute_step(uint32_t st, int u, int wn0, int wm
       wn = read_frag<G>(bw + in * P::kGrpBytes + kn * kSliceOff);
       wsn = lds_read<uint8_t>(sw + in * kRowGroup * kStepBlocks + 2 * kn);
     }
+    // keep the next fragment's read ahead of these MFMAs (left alone, the
+    // scheduler sinks it below them to reuse the registers, and its latency
+    // lands in front of the next MFMA)
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < TM; ++j) MM_MFMA32_GROUP(G, acc[i][j], wf, xf[kk][j], ws, xs[kk][j]);
     wf = wn;
