@@ -337,8 +337,14 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
   run_group<1, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc);
   run_group<2, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc);
 
-  // lane 32 g + r, register q: output column n = 8 (q/4) + 4 g + q%4 of the
-  // fragment, output row m = r
+  // Epilogue: the bf16 tile is assembled in LDS (free again after the last
+  // group's closing barrier) and written out as whole rows, 16 bytes per
+  // lane, so every store fills full cache lines.  Lane 32 g + r, register q
+  // holds output column n = 8 (q/4) + 4 g + q%4 of its fragment and output
+  // row m = r.  Rows are padded by 16 bytes: the fragment writes of 32 lanes
+  // (32 rows) then fall on distinct banks.
+  constexpr int kRowStride = BN * 2 + 16;
+  static_assert(BM * kRowStride <= kLdsBytes, "epilogue tile fits LDS");
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5, r = lane & 31;
 #pragma unroll
@@ -347,9 +353,27 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
     for (int j = 0; j < SH::TM; ++j)
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
-        const v4f c = {acc[i][j][4 * h], acc[i][j][4 * h + 1], acc[i][j][4 * h + 2], acc[i][j][4 * h + 3]};
-        store_out4(a, m0 + wm0 + 32 * j + r, n0 + wn0 + 32 * i + 8 * h + 4 * g, c, a.x.rows, a.w.rows);
+        const uint32_t lo = f32_to_bf16_rne(acc[i][j][4 * h]) | (f32_to_bf16_rne(acc[i][j][4 * h + 1]) << 16);
+        const uint32_t hi = f32_to_bf16_rne(acc[i][j][4 * h + 2]) | (f32_to_bf16_rne(acc[i][j][4 * h + 3]) << 16);
+        const uint32_t at = lds0 + (wm0 + 32 * j + r) * kRowStride + (wn0 + 32 * i + 8 * h + 4 * g) * 2;
+        *reinterpret_cast<__attribute__((address_space(3))) u32x2*>((uintptr_t)at) = u32x2{lo, hi};
       }
+  __syncthreads();
+  constexpr int kChunks = BN / 8;  // 16-byte chunks per row
+  const int64_t M = a.x.rows, N = a.w.rows;
+  for (int c = threadIdx.x; c < BM * kChunks; c += SH::kThreads) {
+    const int row = c / kChunks, col = (c - row * kChunks) * 8;
+    const int64_t m = m0 + row, n = n0 + col;
+    if (m >= M || n >= N) continue;
+    const u32x4 v = lds_read<u32x4>(lds0 + row * kRowStride + col * 2);
+    uint16_t* dst = a.y + m * a.ldy + n;
+    if (n + 8 <= N) {
+      *reinterpret_cast<u32x4*>(dst) = v;
+    } else {
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+      for (int q = 0; q < (int)(N - n); ++q) dst[q] = (uint16_t)(w[q >> 1] >> (16 * (q & 1)));
+    }
+  }
 }
 
 template <int BN, int BM>
