@@ -159,6 +159,7 @@ __device__ __forceinline__ Dma<G, BN, BM> make_dma(const GemmArgs& a, int64_t n0
 template <int G, int BN, int BM>
 __device__ __forceinline__ void issue(const Dma<G, BN, BM>& d, uint32_t st, int wave, int lane, int p) {
   using P = Plan<G, BN, BM>;
+  p = __builtin_amdgcn_readfirstlane(p);  // wave-uniform: the bases below must be scalar
   const int64_t s = p / P::US;
   const int u = p % P::US;
   const uint8_t* cw = d.code[0] + s * d.rp[0] * P::RB + u * P::kGrpBytes;
@@ -263,9 +264,38 @@ __device__ __forceinline__ void compute_step(uint32_t st, int u, int wn0, int wm
   }
 }
 
+// A group's first sub-step issued ahead, during the previous group's last
+// one: which group (-1: none) and the ring rotation it was placed with.
+struct Ahead {
+  int group;
+  int rot;
+};
+
+// Issue sub-step 0 of group G into a stage of its ring that does not overlap
+// the live bytes [live, live + live_bytes) of the group still computing, and
+// record the ring rotation that puts it there.
+template <int G, int BN, int BM>
+__device__ __forceinline__ void issue_first(const GemmArgs& a, uint32_t lds0, int64_t n0, int64_t m0, int wave,
+                                            uint32_t live, uint32_t live_bytes, Ahead& ah) {
+  using P = Plan<G, BN, BM>;
+  int rot = 0;
+  for (int k = 0; k < P::kStages; ++k) {
+    const uint32_t lo = k * P::kStageBytes, hi = lo + P::kStageBytes;
+    if (hi <= live || lo >= live + live_bytes) {
+      rot = k;
+      break;
+    }
+  }
+  rot = __builtin_amdgcn_readfirstlane(rot);  // uniform; keeps the DMA's M0 value scalar
+  const Dma<G, BN, BM> d = make_dma<G, BN, BM>(a, n0, m0, wave, threadIdx.x & 63);
+  issue<G, BN, BM>(d, lds0 + rot * P::kStageBytes, wave, threadIdx.x & 63, 0);
+  ah.group = G;
+  ah.rot = rot;
+}
+
 template <int G, int BN, int BM>
 __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int64_t n0, int64_t m0, int wave,
-                                          int wn0, int wm0, Acc<BN, BM>& acc) {
+                                          int wn0, int wm0, Acc<BN, BM>& acc, Ahead& ah) {
   using P = Plan<G, BN, BM>;
   constexpr int NS = P::kStages;
   const int S = a.steps[G];
@@ -273,9 +303,14 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
   const int PS = S * P::US;  // sub-steps
   const int lane = threadIdx.x & 63;
   const Dma<G, BN, BM> d = make_dma<G, BN, BM>(a, n0, m0, wave, lane);
+  // sub-step q lives in stage (q + rot) % NS; sub-step 0 may already be in
+  // flight (issued during the previous group's last sub-step)
+  const bool first_ahead = ah.group == G;
+  const int rot = __builtin_amdgcn_readfirstlane(first_ahead ? ah.rot : 0);
+  auto stage = [&](int q) { return lds0 + (uint32_t)__builtin_amdgcn_readfirstlane(((q + rot) % NS) * P::kStageBytes); };
 
-  for (int q = 0; q < NS - 1; ++q)
-    if (q < PS) issue<G, BN, BM>(d, lds0 + q * P::kStageBytes, wave, lane, q);
+  for (int q = first_ahead ? 1 : 0; q < NS - 1; ++q)
+    if (q < PS) issue<G, BN, BM>(d, stage(q), wave, lane, q);
 
   for (int p = 0; p < PS; ++p) {
     // sub-steps p+1 .. p+NS-2 may still be in flight; sub-step p must have
@@ -285,9 +320,21 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
     else
       wait_vmcnt<0>();
     barrier();  // everyone's sub-step-p data is in LDS; everyone is done with p-1
-    // refill the stage that sub-step p-1 used, then multiply sub-step p
-    if (p + NS - 1 < PS) issue<G, BN, BM>(d, lds0 + ((p + NS - 1) % NS) * P::kStageBytes, wave, lane, p + NS - 1);
-    compute_step<G, BN, BM>(lds0 + (p % NS) * P::kStageBytes, p % P::US, wn0, wm0, acc);
+    // refill the stage that sub-step p-1 used; during the last sub-step,
+    // start the next non-empty group instead
+    if (p + NS - 1 < PS) {
+      issue<G, BN, BM>(d, stage(p + NS - 1), wave, lane, p + NS - 1);
+    } else if (p == PS - 1) {
+      const uint32_t live = ((p + rot) % NS) * P::kStageBytes;
+      if constexpr (G < 2) {
+        if (a.steps[G + 1] > 0)
+          issue_first<G + 1, BN, BM>(a, lds0, n0, m0, wave, live, P::kStageBytes, ah);
+        else if constexpr (G == 0) {
+          if (a.steps[2] > 0) issue_first<2, BN, BM>(a, lds0, n0, m0, wave, live, P::kStageBytes, ah);
+        }
+      }
+    }
+    compute_step<G, BN, BM>(stage(p), p % P::US, wn0, wm0, acc);
   }
   // the next group lays its stages out differently: every wave must be done
   // reading this group's LDS first
@@ -333,9 +380,10 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-  run_group<0, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc);
-  run_group<1, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc);
-  run_group<2, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc);
+  Ahead ah{-1, 0};
+  run_group<0, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<1, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<2, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
 
   // Epilogue: the bf16 tile is assembled in LDS (free again after the last
   // group's closing barrier) and written out as whole rows, 16 bytes per
