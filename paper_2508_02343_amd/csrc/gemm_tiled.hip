@@ -30,17 +30,18 @@ namespace tiled {
 
 constexpr int kLdsBytes = 160 * 1024;
 
-// Wavefronts per workgroup, in a 2 x (NW/2) grid: 256 x 256 tiles use eight
-// (two per SIMD: while one waits at a barrier or for LDS, the other's MFMAs
-// run; each holds 128 x 64 outputs, 128 accumulator registers), 256 x 128
-// tiles use four (128 x 64 each).
-__host__ __device__ constexpr int tile_waves(int BN, int BM) { return BN * BM >= 256 * 256 ? 8 : 4; }
+// Eight wavefronts per workgroup, two per SIMD (while one waits at a barrier
+// or for LDS, the other's MFMAs run), all of them issuing the tile's DMA, in
+// a GN x GM grid with 64 activation rows each: 256 x 256 tiles give 128 x 64
+// outputs per wavefront (128 accumulator registers), 256 x 128 tiles 64 x 64.
+__host__ __device__ constexpr int tile_waves(int, int) { return 8; }
 template <int BN, int BM>
 struct Shape {
   static constexpr int NW = tile_waves(BN, BM);
   static constexpr int kThreads = 64 * NW;
-  static constexpr int WN = BN / 2, WM = BM / (NW / 2);  // wavefront tile
-  static constexpr int TN = WN / 32, TM = WM / 32;       // 32-row fragments per wavefront
+  static constexpr int WM = 64, GM = BM / WM, GN = NW / GM, WN = BN / GN;  // wavefront grid and tile
+  static constexpr int TN = WN / 32, TM = WM / 32;                         // 32-row fragments per wavefront
+  static_assert(GN * GM == NW && WN % 32 == 0, "wavefront grid");
 };
 
 // Pipeline plan of group G for a BN x BM tile: a "sub-step" is a whole layout
@@ -60,9 +61,13 @@ struct Plan {
   static constexpr int kStages = kLdsBytes / kStageBytes > 8 ? 8 : kLdsBytes / kStageBytes;
   static constexpr int kWInstr = kWBytes / 1024;            // DMA instructions carrying weight codes
   static constexpr int NW = Shape<BN, BM>::NW;
-  static constexpr int kCodeLoads = kCodeBytes / 1024 / NW;  // per wavefront
-  static constexpr int kLoads = kCodeLoads + 1;             // + the scale words
-  static_assert(kCodeBytes % (1024 * NW) == 0 && kWBytes % 1024 == 0, "DMA instructions must split evenly");
+  // DMA instruction i (1 KB each) belongs to wavefront i % NW: the first kRem
+  // wavefronts issue kCodeLoads of them per sub-step, the others one fewer
+  static constexpr int kInstr = kCodeBytes / 1024;
+  static constexpr int kCodeLoads = (kInstr + NW - 1) / NW;
+  static constexpr int kRem = kInstr % NW;
+  static constexpr int kLoads = kCodeLoads + 1;  // + the scale words (most for any wavefront)
+  static_assert(kCodeBytes % 1024 == 0 && kWBytes % 1024 == 0, "whole DMA instructions");
   static_assert(kStages >= 3, "ring of at least three stages");
   static_assert((kStages - 2) * kLoads < 64, "vmcnt range");
 };
@@ -129,7 +134,8 @@ __device__ __forceinline__ Dma<G, BN, BM> make_dma(const GemmArgs& a, int64_t n0
   const int last_x = (int)(a.x.rp / kRowGroup - m0 / kRowGroup - 1);
 #pragma unroll
   for (int k = 0; k < P::kCodeLoads; ++k) {
-    const int inst = wave * P::kCodeLoads + k;
+    int inst = k * P::NW + wave;
+    inst = inst < P::kInstr ? inst : P::kInstr - 1;  // (not issued)
     const bool op = inst >= P::kWInstr;
     const int q = (inst - (op ? P::kWInstr : 0)) * 1024 + lane * 16;  // byte within the operand's tile slice
     int grp = q / P::kGrpBytes;
@@ -166,8 +172,8 @@ __device__ __forceinline__ void issue(const Dma<G, BN, BM>& d, uint32_t st, int 
   const uint8_t* cx = d.code[1] + s * d.rp[1] * P::RB + u * P::kGrpBytes;
 #pragma unroll
   for (int k = 0; k < P::kCodeLoads; ++k) {
-    const int inst = wave * P::kCodeLoads + k;
-    dma16_s(d.off[k], inst >= P::kWInstr ? cx : cw, st + inst * 1024);
+    const int inst = k * P::NW + wave;
+    if (P::kRem == 0 || inst < P::kInstr) dma16_s(d.off[k], inst >= P::kWInstr ? cx : cw, st + inst * 1024);
   }
   constexpr int H = P::NW / 2;
   const bool op = wave >= H;
@@ -315,10 +321,14 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
   for (int p = 0; p < PS; ++p) {
     // sub-steps p+1 .. p+NS-2 may still be in flight; sub-step p must have
     // landed
-    if (p + NS - 2 < PS)
-      wait_vmcnt<(NS - 2) * P::kLoads>();
-    else
+    if (p + NS - 2 < PS) {
+      if (P::kRem == 0 || wave < P::kRem)
+        wait_vmcnt<(NS - 2) * P::kLoads>();
+      else
+        wait_vmcnt<(NS - 2) * (P::kLoads - 1)>();
+    } else {
       wait_vmcnt<0>();
+    }
     barrier();  // everyone's sub-step-p data is in LDS; everyone is done with p-1
     // refill the stage that sub-step p-1 used; during the last sub-step,
     // start the next non-empty group instead
@@ -368,8 +378,8 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
   const int64_t n0 = (int64_t)tn * BN, m0 = (int64_t)tm * BM;
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: keeps DMA setup scalar
-  const int wn0 = (wave & 1) * SH::WN;
-  const int wm0 = (wave >> 1) * SH::WM;
+  const int wn0 = (wave % SH::GN) * SH::WN;
+  const int wm0 = (wave / SH::GN) * SH::WM;
   const uint32_t lds0 = lds_addr(lds);
 
   Acc<BN, BM> acc;
