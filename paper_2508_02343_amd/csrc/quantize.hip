@@ -83,16 +83,21 @@ __device__ __forceinline__ void zero_tail(const QuantArgs& a, int64_t step, int6
 // past a.rows are padding and quantise an all-zero block.  The thread that
 // owns a group's last block also zeroes the padding blocks of that step.
 template <int kStage>
-__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, const QuantArgs& a, int64_t n,
-                                               int b, int gstep0) {
-  // gather: the block's 32 permuted channels as 16 packed bf16 pairs
+__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, bool last, const QuantArgs& a,
+                                               int64_t n, int b, int gstep0) {
+  // gather: the block's 32 permuted channels, all reads issued before any
+  // is used, then packed as 16 bf16 pairs
+  uint16_t e[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) e[i] = lds_u16(addr[i] + kStage * kStageOff);
+  __builtin_amdgcn_sched_barrier(0);
   uint32_t d[16];
   const bool pad_row = n >= a.rows;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     u16x2 v;
-    v.x = lds_u16(addr[2 * i] + kStage * kStageOff);
-    v.y = lds_u16(addr[2 * i + 1] + kStage * kStageOff);
+    v.x = e[2 * i];
+    v.y = e[2 * i + 1];
     d[i] = pad_row ? 0u : __builtin_bit_cast(uint32_t, v);
   }
 
@@ -118,7 +123,6 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
   const int64_t step = b >> 2;
   const int j = b & 3;
   const int64_t gstep = gstep0 + step;
-  const bool last = b == a.nb[group] - 1;
   if (group == 0) {
     uint32_t w[4];
 #pragma unroll
@@ -204,6 +208,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   const int group = blk < a.nb[0] ? 0 : (blk < a.nb[0] + a.nb[1] ? 1 : 2);
   const int b = blk - (group >= 1 ? a.nb[0] : 0) - (group >= 2 ? a.nb[1] : 0);  // block within its group
   const int gstep0 = (group >= 1 ? a.steps[0] : 0) + (group >= 2 ? a.steps[1] : 0);
+  const bool last = b == (group == 0 ? a.nb[0] : (group == 1 ? a.nb[1] : a.nb[2])) - 1;  // the group's last block
 
   // 16-byte chunk c of a pass lies in pass-row c / (K/8); rows past the end
   // are read from the last row (their results are never stored) and chunks
@@ -256,9 +261,9 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
     const int64_t row = q * rpp + prow;
     if (active && row < a.rp) {
       if ((i & 1) == 0)
-        quantize_block<0>(addr, group, a, row, b, gstep0);
+        quantize_block<0>(addr, group, last, a, row, b, gstep0);
       else
-        quantize_block<1>(addr, group, a, row, b, gstep0);
+        quantize_block<1>(addr, group, last, a, row, b, gstep0);
     }
     if (more) MM_STORE_PASS((i + 1) & 1);
     __syncthreads();

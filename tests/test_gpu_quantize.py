@@ -153,3 +153,17 @@ def test_padding_is_written_as_zero(rows, split):
     b.quantize_act(to_dev_bf16(bits), to_dev_perm(perm), split, out=out)
     torch.cuda.synchronize()
     assert_codes_equal(out, O.quantize_mixed(bits, perm, split), ctx="padding")
+
+
+@pytest.mark.parametrize("rows", [5, 33])
+def test_wide_rows(rows):
+    """Rows wider than a third of LDS (K = 28672, 56 KB of bf16) take the
+    one-row-per-workgroup path; codes and scales still match the oracle."""
+    split = (20480, 4096, 4096)
+    K = sum(split)
+    note(f"wide rows={rows} K={K}")
+    rng = np.random.default_rng(K + rows)
+    bits = W.f32_to_bf16_bits((rng.standard_normal((rows, K)) * np.exp2(rng.integers(-4, 5, (rows, K)))).astype(np.float32))
+    perm = rng.permutation(K).astype(np.int32)
+    got = _run(bits, perm, split)
+    assert_codes_equal(got, O.quantize_mixed(bits, perm, split), ctx="wide rows")
