@@ -137,6 +137,16 @@ FORMATS = {f.name: f for f in (E2M1, E3M2, E2M3, E4M3, E5M2)}
 
 # The formats MicroMix uses for its three groups (Sec. 4.1 "Quantization").
 PARTITION_FORMATS = (E2M1, E3M2, E4M3)
+# The alternatives its ablation compares (Table "tab:ablation-study-mxfp6-mxfp8"):
+# MXFP6 as E2M3 instead of E3M2, MXFP8 as E5M2 instead of E4M3.
+GROUP_FORMAT_CHOICES = ((E2M1,), (E3M2, E2M3), (E4M3, E5M2))
+
+
+def check_formats(formats) -> tuple:
+    formats = tuple(formats)
+    if len(formats) != 3 or any(f not in choices for f, choices in zip(formats, GROUP_FORMAT_CHOICES)):
+        raise ValueError("formats must be (E2M1, E3M2 | E2M3, E4M3 | E5M2)")
+    return formats
 
 
 # ---------------------------------------------------------------------------
@@ -316,6 +326,7 @@ class MXTensor:
     q8: np.ndarray  # uint8 [rows, p8]
     sc: np.ndarray  # uint8 [rows, K/32], E8M0 bytes (exponent + 127)
     split: tuple[int, int, int]
+    formats: tuple = PARTITION_FORMATS  # element format of each group
 
     @property
     def rows(self) -> int:
@@ -331,12 +342,15 @@ def reorder(x: np.ndarray, perm: np.ndarray) -> np.ndarray:
     return np.asarray(x)[:, np.asarray(perm, dtype=np.int64)]
 
 
-def quantize_mixed(x_bf16_bits: np.ndarray, perm: np.ndarray, split) -> MXTensor:
+def quantize_mixed(x_bf16_bits: np.ndarray, perm: np.ndarray, split, formats=PARTITION_FORMATS) -> MXTensor:
     """Reorder, split into G4/G6/G8 and MX-quantise each group.
 
     x_bf16_bits: uint16 [rows, K] bf16 patterns (finite).  Used unchanged for
     activations (online) and weights (offline, same sigma and split).
+    formats: element format of each group, (E2M1, E3M2, E4M3) by default;
+    the 6-bit group may use E2M3 and the 8-bit group E5M2 instead.
     """
+    f4, f6, f8 = check_formats(formats)
     bits = np.asarray(x_bf16_bits, dtype=np.uint16)
     rows, K = bits.shape
     p4, p6, p8 = check_split(K, split)
@@ -346,9 +360,9 @@ def quantize_mixed(x_bf16_bits: np.ndarray, perm: np.ndarray, split) -> MXTensor
         raise ValueError("input holds Inf or NaN")
     xp = reorder(x, perm)
     g4, g6, g8 = xp[:, :p4], xp[:, p4 : p4 + p6], xp[:, p4 + p6 :]
-    c4, e4 = quantize_blocks(g4, E2M1)
-    c6, e6 = quantize_blocks(g6, E3M2)
-    c8, e8 = quantize_blocks(g8, E4M3)
+    c4, e4 = quantize_blocks(g4, f4)
+    c6, e6 = quantize_blocks(g6, f6)
+    c8, e8 = quantize_blocks(g8, f8)
     e = np.concatenate([e4, e6, e8], axis=1) if K else np.zeros((rows, 0), np.int64)
     return MXTensor(
         q4=pack_fp4(c4),
@@ -356,6 +370,7 @@ def quantize_mixed(x_bf16_bits: np.ndarray, perm: np.ndarray, split) -> MXTensor
         q8=c8.astype(np.uint8),
         sc=(e + 127).astype(np.uint8),
         split=(p4, p6, p8),
+        formats=(f4, f6, f8),
     )
 
 
@@ -371,10 +386,11 @@ def dequantize_mixed(t: MXTensor) -> np.ndarray:
     c4, c6, c8 = element_codes(t)
     e = np.asarray(t.sc, dtype=np.int64)[:, : t.K // BLOCK] - 127
     b4, b6 = p4 // BLOCK, (p4 + p6) // BLOCK
+    f4, f6, f8 = t.formats
     parts = [
-        dequantize_blocks(c4, e[:, :b4], E2M1),
-        dequantize_blocks(c6, e[:, b4:b6], E3M2),
-        dequantize_blocks(c8, e[:, b6:], E4M3),
+        dequantize_blocks(c4, e[:, :b4], f4),
+        dequantize_blocks(c6, e[:, b4:b6], f6),
+        dequantize_blocks(c8, e[:, b6:], f8),
     ]
     return np.concatenate(parts, axis=1)
 
@@ -392,6 +408,8 @@ def gemm_mixed(a: MXTensor, w: MXTensor) -> np.ndarray:
     """
     if a.split != w.split:
         raise ValueError("activation and weight must share the split")
+    if tuple(a.formats) != tuple(w.formats):
+        raise ValueError("activation and weight must share the group formats")
     return dequantize_mixed(a) @ dequantize_mixed(w).T
 
 

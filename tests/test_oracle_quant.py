@@ -129,12 +129,13 @@ def test_split_and_perm_validation():
 # ---- mixed GEMM ------------------------------------------------------------
 
 
-def _quant_pair(rng, M, N, K, split):
+def _quant_pair(rng, M, N, K, split, formats=O.PARTITION_FORMATS):
     perm = rng.permutation(K).astype(np.int32)
     xa = _rand_bf16(rng, (M, K))
     xa[:, perm[-32:]] = W.f32_to_bf16_bits(O.bf16_bits_to_f64(xa[:, perm[-32:]]).astype(np.float32) * 25)
     xw = _rand_bf16(rng, (N, K), 0.02)
-    return O.quantize_mixed(xa, perm, split), O.quantize_mixed(xw, perm, split), xa, xw, perm
+    return (O.quantize_mixed(xa, perm, split, formats), O.quantize_mixed(xw, perm, split, formats), xa, xw,
+            perm)
 
 
 def test_gemm_is_sum_of_partition_gemms():
@@ -225,14 +226,13 @@ def test_brute_force_single_block_32x32(split):
     _brute_force_case(32, 32, 32, split, seed=sum(i * v for i, v in enumerate(split)))
 
 
-def _brute_force_case(M, N, K, split, seed):
+def _brute_force_case(M, N, K, split, seed, fmts=(O.E2M1, O.E3M2, O.E4M3)):
     rng = np.random.default_rng(seed)
-    a, w, xa, xw, perm = _quant_pair(rng, M, N, K, split)
+    a, w, xa, xw, perm = _quant_pair(rng, M, N, K, split, fmts)
     y = O.gemm_mixed(a, w)
     fa = O.bf16_bits_to_f64(xa)[:, perm]
     fw = O.bf16_bits_to_f64(xw)[:, perm]
     bounds = np.cumsum((0,) + tuple(split))
-    fmts = (O.E2M1, O.E3M2, O.E4M3)
 
     def q(rowv):
         out = []
@@ -252,6 +252,67 @@ def _brute_force_case(M, N, K, split, seed):
 def test_brute_force_small(split):
     K = sum(split)
     _brute_force_case(4, 3, K, split, seed=K + split[0])
+
+
+@pytest.mark.parametrize("split", [(0, 32, 0), (0, 0, 32), (32, 32, 32), (0, 64, 32)])
+def test_brute_force_small_alternative_formats(split):
+    """The ablation's alternatives (MXFP6 as E2M3, MXFP8 as E5M2) through the
+    same independent quantiser and exact triple loop."""
+    K = sum(split)
+    _brute_force_case(4, 3, K, split, seed=2 * K + split[1], fmts=(O.E2M1, O.E2M3, O.E5M2))
+
+
+def test_all_fp8_e5m2_split_equals_plain_mxfp8_gemm_via_torch_decode():
+    rng = np.random.default_rng(19)
+    K = 128
+    a, w, *_ = _quant_pair(rng, 6, 5, K, (0, 0, K), (O.E2M1, O.E3M2, O.E5M2))
+    y = O.gemm_mixed(a, w)
+
+    def torch_dq(t):
+        vals = torch.from_numpy(np.ascontiguousarray(t.q8)).view(torch.float8_e5m2).double().numpy()
+        return vals * np.exp2(t.sc.astype(np.int64) - 127).repeat(32, 1)
+
+    np.testing.assert_allclose(y, torch_dq(a) @ torch_dq(w).T, rtol=1e-13, atol=0)
+
+
+def test_all_fp6_e2m3_split_matches_closed_form_lookup_gemm():
+    """E2M3 magnitudes from their closed form (bias 1): m/8 for exponent
+    field 0, (1 + m/8) * 2^(E-1) otherwise; codes unpacked from the 24-byte
+    little-endian stream by hand."""
+    rng = np.random.default_rng(20)
+    K = 64
+    a, w, *_ = _quant_pair(rng, 4, 3, K, (0, K, 0), (O.E2M1, O.E2M3, O.E4M3))
+    mag = [(m / 8 if E == 0 else (1 + m / 8) * 2.0 ** (E - 1)) for E in range(4) for m in range(8)]
+
+    def dq(t):
+        out = np.zeros((t.rows, K))
+        for r in range(t.rows):
+            bits = int.from_bytes(bytes(t.q6[r]), "little")
+            for i in range(K):
+                c = (bits >> (6 * i)) & 63
+                out[r, i] = (-1 if c & 32 else 1) * mag[c & 31] * 2.0 ** (int(t.sc[r, i // 32]) - 127)
+        return out
+
+    np.testing.assert_allclose(O.gemm_mixed(a, w), dq(a) @ dq(w).T, rtol=1e-13, atol=0)
+
+
+def test_group_formats_touch_only_their_group():
+    rng = np.random.default_rng(21)
+    split = (64, 64, 64)
+    K = sum(split)
+    x = _rand_bf16(rng, (5, K), 1.0)
+    perm = rng.permutation(K).astype(np.int32)
+    d = O.quantize_mixed(x, perm, split)
+    v = O.quantize_mixed(x, perm, split, (O.E2M1, O.E2M3, O.E5M2))
+    assert np.array_equal(d.q4, v.q4) and np.array_equal(d.sc[:, :2], v.sc[:, :2])
+    # E2M3 has emax 2 (E3M2 4), E5M2 15 (E4M3 8): the scale bytes move by the difference
+    # unless the clamp at -127 or the all-zero rule applies
+    assert np.all(v.sc[:, 2:4].astype(int) - d.sc[:, 2:4] == 2)
+    assert np.all(d.sc[:, 4:6].astype(int) - v.sc[:, 4:6] == 7)
+    with pytest.raises(ValueError):
+        O.quantize_mixed(x, perm, split, (O.E2M1, O.E4M3, O.E4M3))
+    with pytest.raises(ValueError):
+        O.gemm_mixed(d, v)
 
 
 def test_average_bits_formula():
