@@ -63,7 +63,10 @@
  * rows .. R-1, hold zero codes and scale byte 0; the quantise calls write
  * them and mm_gemm relies on them.
  * Element codes are sign | exponent | mantissa with the OCP MX encodings:
- * E2M1 bias 1, E3M2 bias 3, E4M3 bias 7 (S.1111.111 is NaN and never written).
+ * E2M1 bias 1, E3M2 bias 3, E4M3 bias 7 (S.1111.111 is NaN and never written);
+ * with the alternative formats (mm_formats below) the 6-bit group holds E2M3
+ * codes (bias 1) and the 8-bit group E5M2 codes (bias 15; its Inf and NaN
+ * codes are never written), in the same byte positions.
  * mm_mx_layout_sizes() gives each buffer's byte count.
  * Requirements: K > 0 and K % 32 == 0; p4, p6, p8 >= 0, each % 32 == 0,
  * p4 + p6 + p8 == K; every buffer of a non-empty group 16-byte aligned and
@@ -72,7 +75,8 @@
  *
  * Quantisation rule (bit-exact): for a block with largest magnitude amax the
  * scale exponent is e = floor(log2 amax) - emax, with emax the format's top
- * binade exponent (E2M1 2, E3M2 4, E4M3 8), clamped to [-127, 127], and
+ * binade exponent (E2M1 2, E3M2 4, E2M3 2, E4M3 8, E5M2 15), clamped to
+ * [-127, 127], and
  * e = -127 for an all-zero block.  Each element x is coded as x * 2^-e
  * rounded to the nearest representable value, ties to the even code,
  * saturating at the largest finite value, keeping the sign of x (so -0 and
@@ -87,7 +91,7 @@
 extern "C" {
 #endif
 
-#define MM_ABI_VERSION 2
+#define MM_ABI_VERSION 3
 
 typedef enum {
   MM_OK = 0,
@@ -95,7 +99,7 @@ typedef enum {
   MM_ERR_SHAPE = 2,  /* rows/K/ld out of range, or a/w disagree in mm_gemm  */
   MM_ERR_SPLIT = 3,  /* p4/p6/p8 not multiples of 32, negative, or sum != K */
   MM_ERR_ALIGN = 4,  /* a pointer or leading dimension is misaligned        */
-  MM_ERR_FORMAT = 5, /* reserved for element-format selection               */
+  MM_ERR_FORMAT = 5, /* unknown element format, or a and w formats differ   */
   MM_ERR_DEVICE = 6  /* the HIP runtime reported an error at launch         */
 } mm_status;
 
@@ -103,14 +107,30 @@ typedef struct {
   int32_t p4, p6, p8; /* channels per group: MXFP4, MXFP6, MXFP8 */
 } mm_split;
 
+/*
+ * Element formats of the 6-bit and 8-bit groups (Sec. 4.1 uses E3M2 and
+ * E4M3; its ablation, Table "tab:ablation-study-mxfp6-mxfp8", compares E2M3
+ * and E5M2).  The zero value of each field is the default, so a
+ * zero-initialised descriptor selects E3M2 and E4M3.  Any other value is
+ * rejected with MM_ERR_FORMAT.
+ */
+typedef enum { MM_FP6_E3M2 = 0, MM_FP6_E2M3 = 1 } mm_fp6_format;
+typedef enum { MM_FP8_E4M3 = 0, MM_FP8_E5M2 = 1 } mm_fp8_format;
+
 typedef struct {
-  int64_t rows;   /* M for activations, N for weights            */
-  int64_t K;      /* channels per row                            */
-  mm_split split; /* group sizes, identical for a and w in GEMM  */
-  uint8_t* q4;    /* E2M1 codes (layout above)                    */
-  uint8_t* q6;    /* E3M2 codes                                   */
-  uint8_t* q8;    /* E4M3 codes                                   */
-  uint8_t* sc;    /* E8M0 scales                                  */
+  int32_t fp6; /* mm_fp6_format of the 6-bit group */
+  int32_t fp8; /* mm_fp8_format of the 8-bit group */
+} mm_formats;
+
+typedef struct {
+  int64_t rows;       /* M for activations, N for weights            */
+  int64_t K;          /* channels per row                            */
+  mm_split split;     /* group sizes, identical for a and w in GEMM  */
+  mm_formats formats; /* element formats, identical for a and w      */
+  uint8_t* q4;        /* E2M1 codes (layout above)                    */
+  uint8_t* q6;        /* 6-bit codes (E3M2 or E2M3)                   */
+  uint8_t* q8;        /* 8-bit codes (E4M3 or E5M2)                   */
+  uint8_t* sc;        /* E8M0 scales                                  */
 } mm_mx_tensor;
 
 typedef struct {
@@ -135,7 +155,7 @@ mm_status mm_mx_layout_sizes(int64_t rows, int64_t K, mm_split split, mm_mx_size
  *   out     host descriptor of device buffers, filled as described above
  *           (including the padding).
  * K may be at most 32768.  Errors: MM_ERR_NULL, MM_ERR_SHAPE, MM_ERR_SPLIT,
- * MM_ERR_ALIGN, MM_ERR_DEVICE.
+ * MM_ERR_ALIGN, MM_ERR_FORMAT, MM_ERR_DEVICE.
  */
 mm_status mm_quantize_act(const void* x_bf16, int64_t ldx, const int32_t* perm, const mm_mx_tensor* out,
                           void* stream);
@@ -160,7 +180,8 @@ mm_status mm_quantize_weight(const void* w_bf16, int64_t ldw, const int32_t* per
  *   y_bf16  device, bf16 [M, N] row-major, row stride ldy elements
  *           (ldy >= N, ldy % 8 == 0, 16-byte aligned).
  * Errors: MM_ERR_NULL, MM_ERR_SHAPE (K or split differ, ldy below N),
- * MM_ERR_SPLIT, MM_ERR_ALIGN, MM_ERR_DEVICE.
+ * MM_ERR_SPLIT, MM_ERR_ALIGN, MM_ERR_FORMAT (formats differ or unknown),
+ * MM_ERR_DEVICE.
  */
 mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, int64_t ldy, void* stream);
 

@@ -25,11 +25,22 @@ class MMSplit(ctypes.Structure):
     _fields_ = [("p4", ctypes.c_int32), ("p6", ctypes.c_int32), ("p8", ctypes.c_int32)]
 
 
+class MMFormats(ctypes.Structure):
+    _fields_ = [("fp6", ctypes.c_int32), ("fp8", ctypes.c_int32)]
+
+
+# element formats of the 6-bit and 8-bit groups: name -> mm_fp6_format / mm_fp8_format
+FP6_FORMATS = {"E3M2": 0, "E2M3": 1}
+FP8_FORMATS = {"E4M3": 0, "E5M2": 1}
+DEFAULT_FORMATS = ("E3M2", "E4M3")
+
+
 class MMTensor(ctypes.Structure):
     _fields_ = [
         ("rows", ctypes.c_int64),
         ("K", ctypes.c_int64),
         ("split", MMSplit),
+        ("formats", MMFormats),
         ("q4", ctypes.c_void_p),
         ("q6", ctypes.c_void_p),
         ("q8", ctypes.c_void_p),
@@ -108,9 +119,10 @@ class MXTensor:
     q6: torch.Tensor | None
     q8: torch.Tensor | None
     sc: torch.Tensor
+    formats: tuple[str, str] = DEFAULT_FORMATS  # element formats of the 6-bit and 8-bit groups
 
     @classmethod
-    def empty(cls, rows: int, K: int, split, device="cuda") -> "MXTensor":
+    def empty(cls, rows: int, K: int, split, device="cuda", formats=DEFAULT_FORMATS) -> "MXTensor":
         split = tuple(int(p) for p in split)
         sz = layout_sizes(rows, K, split)
 
@@ -119,12 +131,14 @@ class MXTensor:
                 return None
             return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
-        return cls(rows, K, split, buf(sz["q4"]), buf(sz["q6"]), buf(sz["q8"]), buf(sz["sc"]))
+        return cls(rows, K, split, buf(sz["q4"]), buf(sz["q6"]), buf(sz["q8"]), buf(sz["sc"]), tuple(formats))
 
     def descriptor(self) -> MMTensor:
         d = MMTensor()
         d.rows, d.K = self.rows, self.K
         d.split = MMSplit(*self.split)
+        # unknown names map to -1, which the library rejects (MM_ERR_FORMAT)
+        d.formats = MMFormats(FP6_FORMATS.get(self.formats[0], -1), FP8_FORMATS.get(self.formats[1], -1))
         for name in ("q4", "q6", "q8", "sc"):
             t = getattr(self, name)
             setattr(d, name, t.data_ptr() if t is not None else None)
@@ -138,29 +152,32 @@ class MXTensor:
                 for k in ("q4", "q6", "q8", "sc")}
 
 
-def _quantize(fn, x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None, stream) -> MXTensor:
+def _quantize(fn, x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None, stream, formats) -> MXTensor:
     if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
         raise ValueError("x must be a 2-D row-major bfloat16 tensor")
     if perm.dtype != torch.int32 or not perm.is_contiguous():
         raise ValueError("perm must be a contiguous int32 tensor")
     rows, K = x.shape
     if out is None:
-        out = MXTensor.empty(rows, K, split, device=x.device)
+        out = MXTensor.empty(rows, K, split, device=x.device, formats=formats)
     d = out.descriptor()
     _check(fn(ctypes.c_void_p(x.data_ptr()), x.stride(0), ctypes.c_void_p(perm.data_ptr()), ctypes.byref(d),
               _stream_ptr(stream)))
     return out
 
 
-def quantize_act(x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None = None, stream=None) -> MXTensor:
-    """mm_quantize_act: fused reorder-and-quantize of bf16 activations."""
-    return _quantize(lib.mm_quantize_act, x, perm, split, out, stream)
+def quantize_act(x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None = None, stream=None,
+                 formats=DEFAULT_FORMATS) -> MXTensor:
+    """mm_quantize_act: fused reorder-and-quantize of bf16 activations
+    (formats: of the 6-bit and 8-bit groups, used when out is None)."""
+    return _quantize(lib.mm_quantize_act, x, perm, split, out, stream, formats)
 
 
 def quantize_weight(w: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None = None,
-                    stream=None) -> MXTensor:
-    """mm_quantize_weight: offline reorder-and-quantize of a bf16 weight [N, K]."""
-    return _quantize(lib.mm_quantize_weight, w, perm, split, out, stream)
+                    stream=None, formats=DEFAULT_FORMATS) -> MXTensor:
+    """mm_quantize_weight: offline reorder-and-quantize of a bf16 weight [N, K]
+    (formats as for quantize_act)."""
+    return _quantize(lib.mm_quantize_weight, w, perm, split, out, stream, formats)
 
 
 def gemm(a: MXTensor, w: MXTensor, y: torch.Tensor | None = None, stream=None) -> torch.Tensor:

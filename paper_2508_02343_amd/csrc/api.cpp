@@ -63,11 +63,17 @@ mm_status check_shape(int64_t rows, int64_t K, mm_split s, const char* name) {
   return MM_OK;
 }
 
+// Format set of a descriptor (the kernels' fs): bit 0 E2M3, bit 1 E5M2.
+int format_set(const mm_mx_tensor* t) { return (t->formats.fp6 == MM_FP6_E2M3 ? 1 : 0) | (t->formats.fp8 == MM_FP8_E5M2 ? 2 : 0); }
+
 // Checks shared by both quantise calls and the GEMM.
 mm_status check_tensor(const mm_mx_tensor* t, const char* name) {
   if (!t) return fail(MM_ERR_NULL, "%s: descriptor is NULL", name);
   mm_status st = check_shape(t->rows, t->K, t->split, name);
   if (st != MM_OK) return st;
+  if ((t->formats.fp6 != MM_FP6_E3M2 && t->formats.fp6 != MM_FP6_E2M3) ||
+      (t->formats.fp8 != MM_FP8_E4M3 && t->formats.fp8 != MM_FP8_E5M2))
+    return fail(MM_ERR_FORMAT, "%s: unknown element format (fp6=%d, fp8=%d)", name, t->formats.fp6, t->formats.fp8);
   const Layout l = layout(t->rows, t->split);
   const uint8_t* ptrs[4] = {t->q4, t->q6, t->q8, t->sc};
   const char* what[4] = {"q4", "q6", "q8", "sc"};
@@ -106,6 +112,7 @@ mm_status quantize(const void* x, int64_t ldx, const int32_t* perm, const mm_mx_
   a.q[1] = out->q6;
   a.q[2] = out->q8;
   a.sc = out->sc;
+  a.fs = format_set(out);
   hipError_t e = mm::launch_quantize(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "%s: launch failed: %s", who, hipGetErrorString(e));
   return MM_OK;
@@ -146,6 +153,7 @@ mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, in
   if (a->K != w->K) return fail(MM_ERR_SHAPE, "mm_gemm: K differs (%lld vs %lld)", (long long)a->K, (long long)w->K);
   if (a->split.p4 != w->split.p4 || a->split.p6 != w->split.p6 || a->split.p8 != w->split.p8)
     return fail(MM_ERR_SHAPE, "mm_gemm: a and w must share the split");
+  if (format_set(a) != format_set(w)) return fail(MM_ERR_FORMAT, "mm_gemm: a and w must share the element formats");
   if (ldy < w->rows) return fail(MM_ERR_SHAPE, "mm_gemm: ldy=%lld below N=%lld", (long long)ldy, (long long)w->rows);
   if (!aligned16(y_bf16) || ldy % 8 != 0) return fail(MM_ERR_ALIGN, "mm_gemm: y must be 16-byte aligned with ldy %% 8 == 0");
   mm::GemmArgs g;
@@ -155,6 +163,7 @@ mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, in
   for (int k = 0; k < 3; ++k) g.steps[k] = l.steps[k];
   g.y = static_cast<uint16_t*>(y_bf16);
   g.ldy = ldy;
+  g.fs = format_set(a);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = a->rows <= kDirectMaxM ? mm::launch_gemm_direct(g, s) : mm::launch_gemm_tiled(g, s);
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "mm_gemm: launch failed: %s", hipGetErrorString(e));

@@ -41,7 +41,12 @@ __device__ __forceinline__ uint2 gload8(const void* p) {
 }
 
 // MFMA format selector of a group.
-__host__ __device__ constexpr int group_fmt(int group) { return group == 0 ? kE2M1 : (group == 1 ? kE3M2 : kE4M3); }
+// MFMA format selector of a group under format set fs (bit 0: the 6-bit
+// group is E2M3 instead of E3M2; bit 1: the 8-bit group is E5M2 instead of
+// E4M3).
+__host__ __device__ constexpr int group_fmt(int group, int fs) {
+  return group == 0 ? kE2M1 : (group == 1 ? ((fs & 1) ? kE2M3 : kE3M2) : ((fs & 2) ? kE5M2 : kE4M3));
+}
 
 // One lane's 16 x 128 operand fragment (16 x 16 x 128 form, lane 16 g + r)
 // straight from the packed layout: row n, step `step` of group G.  The padded
@@ -92,9 +97,9 @@ __device__ __forceinline__ int load_scale(const uint8_t* sc, int64_t rp, int64_t
 // acc = acc + A(group G) x B(group G) with per-block E8M0 scales sa / sb.
 // The format selectors must reach the builtin as integer constants (they are
 // instruction immediates), hence the constexpr locals.
-#define MM_MFMA_GROUP(G, acc, a, b, sa, sb)                                                         \
+#define MM_MFMA_GROUP(G, FS, acc, a, b, sa, sb)                                                     \
   do {                                                                                              \
-    constexpr int mm_fmt_ = group_fmt(G);                                                           \
+    constexpr int mm_fmt_ = group_fmt(G, FS);                                                       \
     (acc) = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4((a), (b), (acc), mm_fmt_, mm_fmt_, 0, \
                                                              (sa), 0, (sb));                        \
   } while (0)
@@ -107,9 +112,9 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 // (row r, block b) comes from lane 32 b + r.  Result: lane 32 g + r,
 // register q holds C[8 (q/4) + 4 g + q%4][r].  On gfx950 this form runs E2M1
 // and E3M2 well above the 16 x 16 x 128 form's rate.
-#define MM_MFMA32_GROUP(G, acc, a, b, sa, sb)                                                       \
+#define MM_MFMA32_GROUP(G, FS, acc, a, b, sa, sb)                                                   \
   do {                                                                                              \
-    constexpr int mm_fmt_ = group_fmt(G);                                                           \
+    constexpr int mm_fmt_ = group_fmt(G, FS);                                                       \
     (acc) = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4((a), (b), (acc), mm_fmt_, mm_fmt_, 0,  \
                                                             (sa), 0, (sb));                         \
   } while (0)

@@ -10,7 +10,7 @@ namespace mm {
 
 constexpr int kDirectWaves = 4;
 
-template <int TN, int TM, int G>
+template <int TN, int TM, int G, int FS>
 __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][TM], int64_t n0, int64_t m0,
                                              int wave, int lane) {
   const int S = a.steps[G];
@@ -38,11 +38,11 @@ __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][T
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
-      for (int j = 0; j < TM; ++j) MM_MFMA_GROUP(G, acc[i][j], wf[i], xf[j], ws[i], xs[j]);
+      for (int j = 0; j < TM; ++j) MM_MFMA_GROUP(G, FS, acc[i][j], wf[i], xf[j], ws[i], xs[j]);
   }
 }
 
-template <int TN, int TM>
+template <int TN, int TM, int FS>
 __global__ __launch_bounds__(64 * kDirectWaves) void gemm_direct_kernel(GemmArgs a) {
   __shared__ float red[kDirectWaves - 1][TN * TM * 4][64];
   const int lane = threadIdx.x & 63;
@@ -56,9 +56,9 @@ __global__ __launch_bounds__(64 * kDirectWaves) void gemm_direct_kernel(GemmArgs
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  direct_group<TN, TM, 0>(a, acc, n0, m0, wave, lane);
-  direct_group<TN, TM, 1>(a, acc, n0, m0, wave, lane);
-  direct_group<TN, TM, 2>(a, acc, n0, m0, wave, lane);
+  direct_group<TN, TM, 0, FS>(a, acc, n0, m0, wave, lane);
+  direct_group<TN, TM, 1, FS>(a, acc, n0, m0, wave, lane);
+  direct_group<TN, TM, 2, FS>(a, acc, n0, m0, wave, lane);
 
   if (wave > 0) {
 #pragma unroll
@@ -84,11 +84,23 @@ __global__ __launch_bounds__(64 * kDirectWaves) void gemm_direct_kernel(GemmArgs
     }
 }
 
+template <int TN, int TM, int FS>
+static hipError_t launch_direct_fs(const GemmArgs& a, hipStream_t stream) {
+  const dim3 grid((unsigned)((a.w.rows + 16 * TN - 1) / (16 * TN)), (unsigned)((a.x.rows + 16 * TM - 1) / (16 * TM)));
+  hipLaunchKernelGGL((gemm_direct_kernel<TN, TM, FS>), grid, dim3(64 * kDirectWaves), 0, stream, a);
+  return hipGetLastError();
+}
+
+// The format set is an instruction immediate: one kernel per set.
 template <int TN, int TM>
 static hipError_t launch_direct(const GemmArgs& a, hipStream_t stream) {
-  const dim3 grid((unsigned)((a.w.rows + 16 * TN - 1) / (16 * TN)), (unsigned)((a.x.rows + 16 * TM - 1) / (16 * TM)));
-  hipLaunchKernelGGL((gemm_direct_kernel<TN, TM>), grid, dim3(64 * kDirectWaves), 0, stream, a);
-  return hipGetLastError();
+  switch (a.fs) {
+    case 0: return launch_direct_fs<TN, TM, 0>(a, stream);
+    case 1: return launch_direct_fs<TN, TM, 1>(a, stream);
+    case 2: return launch_direct_fs<TN, TM, 2>(a, stream);
+    case 3: return launch_direct_fs<TN, TM, 3>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_gemm_direct(const GemmArgs& a, hipStream_t stream) {

@@ -225,7 +225,7 @@ using Acc = v16f[Shape<BN, BM>::TN][Shape<BN, BM>::TM];
 // All activation fragments of the sub-step are read first; weight fragments
 // are double-buffered: the next one is read while the MFMAs of the current
 // one run.
-template <int G, int BN, int BM>
+template <int G, int BN, int BM, int FS>
 __device__ __forceinline__ void compute_step(uint32_t st, int u, int wn0, int wm0, Acc<BN, BM>& acc) {
   using P = Plan<G, BN, BM>;
   constexpr int TN = Shape<BN, BM>::TN, TM = Shape<BN, BM>::TM, SL = P::kSlices;
@@ -264,7 +264,7 @@ __device__ __forceinline__ void compute_step(uint32_t st, int u, int wn0, int wm
     // lands in front of the next MFMA)
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < TM; ++j) MM_MFMA32_GROUP(G, acc[i][j], wf, xf[kk][j], ws, xs[kk][j]);
+    for (int j = 0; j < TM; ++j) MM_MFMA32_GROUP(G, FS, acc[i][j], wf, xf[kk][j], ws, xs[kk][j]);
     wf = wn;
     ws = wsn;
   }
@@ -299,7 +299,7 @@ __device__ __forceinline__ void issue_first(const GemmArgs& a, uint32_t lds0, in
   ah.rot = rot;
 }
 
-template <int G, int BN, int BM>
+template <int G, int BN, int BM, int FS>
 __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int64_t n0, int64_t m0, int wave,
                                           int wn0, int wm0, Acc<BN, BM>& acc, Ahead& ah) {
   using P = Plan<G, BN, BM>;
@@ -344,7 +344,7 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
         }
       }
     }
-    compute_step<G, BN, BM>(stage(p), p % P::US, wn0, wm0, acc);
+    compute_step<G, BN, BM, FS>(stage(p), p % P::US, wn0, wm0, acc);
   }
   // the next group lays its stages out differently: every wave must be done
   // reading this group's LDS first
@@ -356,7 +356,7 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
 
 using namespace tiled;
 
-template <int BN, int BM>
+template <int BN, int BM, int FS>
 __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(GemmArgs a, int tiles_n, int tiles_m) {
   using SH = Shape<BN, BM>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
@@ -391,9 +391,9 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
   Ahead ah{-1, 0};
-  run_group<0, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
-  run_group<1, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
-  run_group<2, BN, BM>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<0, BN, BM, FS>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<1, BN, BM, FS>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<2, BN, BM, FS>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
 
   // Epilogue: the bf16 tile is assembled in LDS (free again after the last
   // group's closing barrier) and written out as whole rows, 16 bytes per
@@ -434,19 +434,31 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
   }
 }
 
-template <int BN, int BM>
-static hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
+template <int BN, int BM, int FS>
+static hipError_t launch_tile_fs(const GemmArgs& a, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel<BN, BM>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel<BN, BM, FS>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int tn = (int)((a.w.rows + BN - 1) / BN), tm = (int)((a.x.rows + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads), kLdsBytes, stream, a,
+  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM, FS>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads), kLdsBytes, stream, a,
                      tn, tm);
   return hipGetLastError();
+}
+
+// The format set is an instruction immediate: one kernel per set.
+template <int BN, int BM>
+static hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
+  switch (a.fs) {
+    case 0: return launch_tile_fs<BN, BM, 0>(a, stream);
+    case 1: return launch_tile_fs<BN, BM, 1>(a, stream);
+    case 2: return launch_tile_fs<BN, BM, 2>(a, stream);
+    case 3: return launch_tile_fs<BN, BM, 3>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t stream) {

@@ -39,6 +39,7 @@ struct QuantArgs {
   int steps[3];  // steps per group
   uint8_t* q[3];
   uint8_t* sc;
+  int fs;  // format set: bit 0 the 6-bit group is E2M3 (else E3M2), bit 1 the 8-bit group is E5M2 (else E4M3)
 };
 
 // One quantised GEMM operand.
@@ -55,6 +56,7 @@ struct GemmArgs {
   int steps[3];  // steps per group
   uint16_t* y;
   int64_t ldy;
+  int fs;  // format set of both operands (as QuantArgs::fs)
 };
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream);

@@ -114,7 +114,8 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
   // Shared exponent e = floor(log2 amax) - emax, clamped below at -127: for
   // a bf16 amax with biased exponent E this is max(E - 127 - emax, -127); a
   // subnormal or zero amax (E = 0) lands on the clamp.  The E8M0 byte is e+127.
-  const int emax = group == 0 ? 2 : (group == 1 ? 4 : 8);
+  const bool e2m3 = (a.fs & 1) != 0, e5m2 = (a.fs & 2) != 0;  // the alternative formats of groups 1 and 2
+  const int emax = group == 0 ? 2 : (group == 1 ? (e2m3 ? 2 : 4) : (e5m2 ? 15 : 8));
   const int E = (int)(amax >> 7);
   const uint32_t sbyte = (uint32_t)(E - emax > 0 ? E - emax : 0);
   // the conversions read the scale's E8M0 exponent from an fp32 operand
@@ -138,17 +139,30 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
     if (last) zero_tail<0>(a, step, gstep, n, j);
   } else if (group == 1) {
     u32x16 v;
+    i32x6 c;
+    if (e2m3) {
+      // clamp the magnitudes to the largest E2M3 value, 7.5 * 2^e (exact in
+      // bf16: biased exponent e + 129 = sbyte + 2, mantissa 0x70), keep the
+      // signs; nothing then depends on how the conversion treats larger values
+      const uint32_t lim = ((sbyte + 2u) << 7) | 0x70u;
+      const uint32_t lim2 = lim | (lim << 16);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] = d[i];
-    const i32x6 c = __builtin_amdgcn_cvt_scalef32_pk32_bf6_bf16(__builtin_bit_cast(bf16x32, v), scale);
+      for (int i = 0; i < 16; ++i) v[i] = min_u16x2(d[i] & 0x7FFF7FFFu, lim2) | (d[i] & 0x80008000u);
+      c = __builtin_amdgcn_cvt_scalef32_pk32_fp6_bf16(__builtin_bit_cast(bf16x32, v), scale);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] = d[i];
+      c = __builtin_amdgcn_cvt_scalef32_pk32_bf6_bf16(__builtin_bit_cast(bf16x32, v), scale);
+    }
     uint2* dst = reinterpret_cast<uint2*>(a.q[1] + code_offset<1>(step, a.rp, n, j));
     dst[0] = make_uint2((uint32_t)c[0], (uint32_t)c[1]);
     dst[1] = make_uint2((uint32_t)c[2], (uint32_t)c[3]);
     dst[2] = make_uint2((uint32_t)c[4], (uint32_t)c[5]);
     if (last) zero_tail<1>(a, step, gstep, n, j);
   } else {
-    // 448 * 2^e in bf16: biased exponent e + 127 + 8 = sbyte + 8, mantissa 0x60
-    const uint32_t lim = ((sbyte + 8u) << 7) | 0x60u;
+    // the largest finite value times 2^e in bf16, mantissa 0x60 (1.75): E4M3
+    // 448 (biased exponent e + 127 + 8 = sbyte + 8), E5M2 57344 (sbyte + 15)
+    const uint32_t lim = ((sbyte + (e5m2 ? 15u : 8u)) << 7) | 0x60u;
     const uint32_t lim2 = lim | (lim << 16);
     uint32_t w[8];
 #pragma unroll
@@ -157,8 +171,13 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
       const uint32_t c0 = min_u16x2(d[2 * q] & 0x7FFF7FFFu, lim2) | (d[2 * q] & 0x80008000u);
       const uint32_t c1 = min_u16x2(d[2 * q + 1] & 0x7FFF7FFFu, lim2) | (d[2 * q + 1] & 0x80008000u);
       i16x2 v = {0, 0};
-      v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c0), scale, false);
-      v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c1), scale, true);
+      if (e5m2) {
+        v = __builtin_amdgcn_cvt_scalef32_pk_bf8_bf16(v, __builtin_bit_cast(bf16x2, c0), scale, false);
+        v = __builtin_amdgcn_cvt_scalef32_pk_bf8_bf16(v, __builtin_bit_cast(bf16x2, c1), scale, true);
+      } else {
+        v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c0), scale, false);
+        v = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(v, __builtin_bit_cast(bf16x2, c1), scale, true);
+      }
       w[q] = __builtin_bit_cast(uint32_t, v);
     }
     uint8_t* dst = a.q[2] + code_offset<2>(step, a.rp, n, j);

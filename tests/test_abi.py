@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(b.LIB_PATH)
     for n in _declared_functions():
         assert hasattr(lib, n), n
-    assert b.lib.mm_abi_version() == 2
+    assert b.lib.mm_abi_version() == 3
 
 
 def test_status_strings():
@@ -72,6 +72,8 @@ def _q(d, x=FAKE, ldx=None, perm=FAKE):
         (lambda d: setattr(d, "sc", None), "MM_ERR_NULL"),
         (lambda d: setattr(d, "q6", FAKE + 8), "MM_ERR_ALIGN"),
         (lambda d: setattr(d, "sc", FAKE + 4), "MM_ERR_ALIGN"),
+        (lambda d: setattr(d, "formats", b.MMFormats(2, 0)), "MM_ERR_FORMAT"),
+        (lambda d: setattr(d, "formats", b.MMFormats(0, -1)), "MM_ERR_FORMAT"),
     ],
 )
 def test_quantize_rejects_bad_descriptors(mutate, expect):
@@ -151,3 +153,30 @@ def test_binding_descriptor_fields():
     assert t.q4.numel() == 2048 and t.sc.numel() == 512
     e = b.MXTensor.empty(3, 64, (64, 0, 0), device="cpu").descriptor()
     assert e.q6 is None and e.q8 is None
+
+
+def test_descriptor_layout_matches_the_header():
+    """The ctypes mirror has the C struct's size and field offsets (checked
+    against a C compiler's view of include/micromix.h)."""
+    import subprocess
+    import tempfile
+
+    src = (f'#include "{HEADER}"\n#include <stddef.h>\n#include <stdio.h>\nint main(void) {{\n'
+           'printf("%zu %zu %zu %zu %zu\\n", sizeof(mm_mx_tensor), offsetof(mm_mx_tensor, split),'
+           ' offsetof(mm_mx_tensor, formats), offsetof(mm_mx_tensor, q4), offsetof(mm_mx_tensor, sc));\n'
+           'return 0; }\n')
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "t.c")
+        open(c, "w").write(src)
+        exe = os.path.join(d, "t")
+        subprocess.run(["gcc", "-std=c99", "-o", exe, c], check=True)
+        got = tuple(int(v) for v in subprocess.run([exe], check=True, capture_output=True, text=True).stdout.split())
+    M = b.MMTensor
+    assert got == (ctypes.sizeof(M), M.split.offset, M.formats.offset, M.q4.offset, M.sc.offset)
+
+
+def test_gemm_rejects_mixed_formats():
+    a, w = _tensor(), _tensor()
+    w.formats = b.MMFormats(1, 0)
+    st = b.lib.mm_gemm(ctypes.byref(a), ctypes.byref(w), ctypes.c_void_p(FAKE), 128, None)
+    assert b.STATUS_NAMES[st] == "MM_ERR_FORMAT"

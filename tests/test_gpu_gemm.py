@@ -114,3 +114,35 @@ def test_one_activation_feeds_two_weights():
     ra = O.quantize_mixed(xb, perm, split)
     assert_gemm_close(y_to_f64(y1), O.gemm_mixed(ra, O.quantize_mixed(wb, perm, split)), "y1")
     assert_gemm_close(y_to_f64(y2), O.gemm_mixed(ra, O.quantize_mixed(wb2, perm, split)), "y2")
+
+
+@pytest.mark.parametrize("formats", [("E2M3", "E5M2"), ("E2M3", "E4M3"), ("E3M2", "E5M2")], ids="-".join)
+@pytest.mark.parametrize("M,N", [(5, 70), (37, 130), (300, 260)])
+def test_alternative_formats(M, N, formats):
+    """The ablation's MXFP6 = E2M3 and MXFP8 = E5M2 variants through both
+    GEMM kernels (decode for M <= 64, tiled above)."""
+    split = (96, 160, 96)
+    note(f"formats {formats} M={M} N={N}")
+    xb, wb, perm = _rand_case(M, N, split, seed=M * 11 + N)
+    b = _b()
+    p = to_dev_perm(perm)
+    a = b.quantize_act(to_dev_bf16(xb), p, split, formats=formats)
+    w = b.quantize_weight(to_dev_bf16(wb), p, split, formats=formats)
+    y = b.gemm(a, w)
+    torch.cuda.synchronize()
+    fm = (O.E2M1, O.FORMATS[formats[0]], O.FORMATS[formats[1]])
+    ra, rw = O.quantize_mixed(xb, perm, split, fm), O.quantize_mixed(wb, perm, split, fm)
+    ctx = f"{formats} M{M} N{N}"
+    assert_codes_equal(a, ra, ctx=ctx + " A")
+    assert_codes_equal(w, rw, ctx=ctx + " W")
+    assert_gemm_close(y_to_f64(y), O.gemm_mixed(ra, rw), ctx=ctx)
+
+
+def test_mixed_formats_are_rejected():
+    xb, wb, perm = _rand_case(8, 16, (96, 160, 96), seed=3)
+    b = _b()
+    p = to_dev_perm(perm)
+    a = b.quantize_act(to_dev_bf16(xb), p, (96, 160, 96), formats=("E2M3", "E4M3"))
+    w = b.quantize_weight(to_dev_bf16(wb), p, (96, 160, 96))
+    with pytest.raises(b.MMError, match="MM_ERR_FORMAT"):
+        b.gemm(a, w)

@@ -167,3 +167,44 @@ def test_wide_rows(rows):
     perm = rng.permutation(K).astype(np.int32)
     got = _run(bits, perm, split)
     assert_codes_equal(got, O.quantize_mixed(bits, perm, split), ctx="wide rows")
+
+
+# The ablation's alternatives (Table tab:ablation-study-mxfp6-mxfp8): MXFP6 as
+# E2M3, MXFP8 as E5M2, alone and together.
+ALT_FORMATS = [("E2M3", "E5M2"), ("E2M3", "E4M3"), ("E3M2", "E5M2")]
+
+
+def _oracle_formats(formats):
+    return (O.E2M1, O.FORMATS[formats[0]], O.FORMATS[formats[1]])
+
+
+@pytest.mark.parametrize("formats", ALT_FORMATS, ids="-".join)
+@pytest.mark.parametrize("split", [(96, 160, 96), (0, 352, 0), (0, 0, 352), (32, 32, 288)])
+def test_alternative_formats_ragged(split, formats):
+    K = sum(split)
+    rows = 37
+    note(f"formats {formats} split={split}")
+    rng = np.random.default_rng(rows * 1000 + split[1] + 7 * split[2])
+    x = (rng.standard_normal((rows, K)) * np.exp2(rng.integers(-3, 4, (rows, K)))).astype(np.float32)
+    bits = W.f32_to_bf16_bits(x)
+    perm = rng.permutation(K).astype(np.int32)
+    b = _b()
+    got = b.quantize_act(to_dev_bf16(bits), to_dev_perm(perm), split, formats=formats)
+    torch.cuda.synchronize()
+    assert_codes_equal(got, O.quantize_mixed(bits, perm, split, _oracle_formats(formats)), ctx=f"{formats} {split}")
+
+
+@pytest.mark.parametrize("formats", ALT_FORMATS, ids="-".join)
+def test_alternative_formats_edge_blocks(formats):
+    """Ties, saturation at each format's top value (7.5 for E2M3, 57344 for
+    E5M2), signed zeros, subnormal inputs and the E8M0 clamp."""
+    split = (128, 96, 64)
+    K = sum(split)
+    note(f"edge blocks formats {formats}")
+    rng = np.random.default_rng(29)
+    bits = _edge_rows(rng, K)
+    b = _b()
+    for perm in (np.arange(K, dtype=np.int32), rng.permutation(K).astype(np.int32)):
+        got = b.quantize_weight(to_dev_bf16(bits), to_dev_perm(perm), split, formats=formats)
+        torch.cuda.synchronize()
+        assert_codes_equal(got, O.quantize_mixed(bits, perm, split, _oracle_formats(formats)), ctx=f"edge {formats}")
