@@ -46,6 +46,12 @@ R12 storage: FP4 two codes per byte (even element in the low nibble); FP6
     four codes per three bytes as a little-endian bit stream (code i at bits
     6i..6i+5 of its 24-byte block); FP8 one code per byte; one E8M0 byte per
     block, row-major, in X' block order.
+R13 calibration: a channel's statistic against the thresholds T(4), T(6) is
+    its mean |X| over the calibration rows (the key sigma sorts by), so every
+    group is a contiguous slice of sigma; max|X| in Ebar_INT8 = max|X| / 254 is
+    taken over the whole calibration tensor; the counts are rounded down to
+    multiples of 32 (channels move to the next wider group, never to a
+    narrower one); T(6) uses the constants of the MXFP6 variant in use.
 """
 
 from __future__ import annotations
@@ -430,3 +436,51 @@ def average_bits(split) -> float:
     p4, p6, p8 = split
     K = p4 + p6 + p8
     return (4 * p4 + 6 * p6 + 8 * p8) / K + 8 / BLOCK
+
+
+# ---------------------------------------------------------------------------
+# Offline calibration (Sec. 3.1 "Offline Channel Assignment Strategy";
+# Def. 1 eq. quantization-threshold; Appendix "Derivations" eq. last)
+# ---------------------------------------------------------------------------
+
+
+def quantization_threshold(fmt: MXFormat, amax_tensor: float) -> float:
+    """T(n) = 2^b * 2^(n-1) / q_max * Ebar_INT8 with Ebar_INT8 = max|X| / 254
+    (the INT8 per-tensor error bound), b the format's exponent bias and q_max
+    its largest value (Table "tab:microscaling")."""
+    return 2.0 ** fmt.bias * 2.0 ** (fmt.bits - 1) / fmt.max_normal * (amax_tensor / 254.0)
+
+
+def channel_abs_mean(x_bf16_bits: np.ndarray) -> np.ndarray:
+    """M_j = (1/L) sum_i |X_ij| over the L calibration rows, float64."""
+    x = bf16_bits_to_f64(np.asarray(x_bf16_bits, dtype=np.uint16))
+    return np.abs(x).sum(axis=0) / x.shape[0]
+
+
+def calibrate(x_bf16_bits: np.ndarray, formats=PARTITION_FORMATS):
+    """(sigma, split) from calibration activations X [L, K] (bf16 patterns).
+
+    sigma: int32 [K], the stable ascending argsort of the channel absolute
+    means M.  split: the group sizes from the thresholds T(4) (E2M1) and T(6)
+    (the MXFP6 format of `formats`) against M under reading R13:
+    p4 = 32 floor(n4/32), p4 + p6 = 32 floor((n4 + n6)/32), p8 the rest.
+    """
+    f4, f6, _ = check_formats(formats)
+    bits = np.asarray(x_bf16_bits, dtype=np.uint16)
+    if bits.ndim != 2:
+        raise ValueError("X must be [L, K]")
+    L, K = bits.shape
+    if L == 0 or K == 0 or K % BLOCK:
+        raise ValueError("need rows > 0 and K a positive multiple of 32")
+    x = bf16_bits_to_f64(bits)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("input holds Inf or NaN")
+    M = np.abs(x).sum(axis=0) / L
+    sigma = np.argsort(M, kind="stable").astype(np.int32)
+    t = float(np.abs(x).max())
+    T4, T6 = quantization_threshold(f4, t), quantization_threshold(f6, t)
+    n4 = int(np.count_nonzero(M <= T4))
+    n6 = int(np.count_nonzero((M > T4) & (M <= T6)))
+    p4 = n4 // BLOCK * BLOCK
+    p46 = (n4 + n6) // BLOCK * BLOCK
+    return sigma, (p4, p46 - p4, K - p46)
