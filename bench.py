@@ -7,7 +7,9 @@ quantisation (mm_quantize_weight) runs once per weight and is timed apart.
 
 Prints one JSON line: whole-step throughput in TFLOP/s (2 M N K per step),
 the GEMM's roofline against the MFMA peak of its bit mix, the quantiser's HBM
-bandwidth, and the CPU oracle timed on the host as a baseline.
+bandwidth, the CPU oracle timed on the host as a baseline, and (outside the
+step) the offline calibration's HBM bandwidth on a calibration set of the
+layer's width.
 
 Inputs are seeded synthetic tensors resident in HBM before the timed region;
 several buffer sets are rotated so the working set exceeds the 256 MB
@@ -117,6 +119,37 @@ def cpu_baseline(w, seconds: float) -> dict:
                       f"{n_iter} iterations in {el:.1f} s"}
 
 
+def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps: int = 10) -> dict:
+    """mm_calibrate over `rows` calibration tokens of the layer's width K
+    (offline, not part of the step): whole-call time with HIP events on the
+    launch stream, and HBM bandwidth over the bytes it must move (X read once,
+    sigma and the split written)."""
+    import torch
+
+    xb = W.calibration_bits(rows, w.K, 1)
+    x0 = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).to(dev)
+    del xb
+    nset = max(1, int(np.ceil(min_set_mb * 1e6 / (rows * w.K * 2))))
+    xs = [x0] + [x0.clone() for _ in range(nset - 1)]
+    ws = torch.empty(B.calibrate_workspace_size(rows, w.K), dtype=torch.uint8, device=dev)
+    perm = torch.empty(w.K, dtype=torch.int32, device=dev)
+    split = torch.empty(3, dtype=torch.int32, device=dev)
+    for i in range(2):
+        B.calibrate_async(xs[i % nset], workspace=ws, perm=perm, split=split, stream=stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(reps):
+        B.calibrate_async(xs[i % nset], workspace=ws, perm=perm, split=split, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = rows * w.K * 2 + w.K * 4 + 12
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": "offline calibration (mm_calibrate, 5 launches)", "rows": rows, "K": w.K, "ms": round(ms, 5),
+            "achieved": round(gbps, 1), "peak": PEAK_HBM, "unit": "GB/s", "frac": round(gbps / PEAK_HBM, 4),
+            "bytes_per_call": nbytes, "split": split.cpu().tolist()}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +159,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--min-working-set-mb", type=float, default=768.0)
+    ap.add_argument("--calibration-rows", type=int, default=32768,
+                    help="calibration tokens for the offline mm_calibrate timing (0 skips it)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -246,6 +281,9 @@ def main() -> int:
         "quant_share_of_kernel_time": round(quant_ms / (quant_ms + gemm_ms), 4),
         "weight_quantize": {"ms": round(wq_ms, 5), "GB/s": round(wq_gbps, 1)},
     }
+    if args.calibration_rows > 0:
+        out["calibration"] = measure_calibration(B, W, w, stream, dev, args.calibration_rows,
+                                                 args.min_working_set_mb)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -13,13 +13,16 @@
  * sums all three partitions in fp32 and writes bfloat16 (Sec. 2.1 eq. 1;
  * Sec. 3.2 "GEMM kernel").
  *
- * Three calls implement that path:
+ * Three calls implement that path, and a fourth prepares it offline:
  *   mm_quantize_act     online fused reorder-and-quantize of activations
  *                       (Sec. 3.2 "Quantization kernel", Fig. "micromix-design" b)
  *   mm_quantize_weight  the same transform for weights, run once offline
  *                       with the activation's sigma and split (Sec. 3.2)
  *   mm_gemm             mixed-precision block-scaled GEMM, Y = A W^T
  *                       (Sec. 3.2 "GEMM kernel", Fig. "micromix-design" a)
+ *   mm_calibrate        offline choice of sigma and the split from
+ *                       calibration activations (Sec. 3.1 "Offline channel
+ *                       assignment strategy"; Def. 1; Appendix C.2 "Derivations")
  *
  * Conventions shared by every call
  * --------------------------------
@@ -91,7 +94,7 @@
 extern "C" {
 #endif
 
-#define MM_ABI_VERSION 3
+#define MM_ABI_VERSION 4
 
 typedef enum {
   MM_OK = 0,
@@ -100,7 +103,8 @@ typedef enum {
   MM_ERR_SPLIT = 3,  /* p4/p6/p8 not multiples of 32, negative, or sum != K */
   MM_ERR_ALIGN = 4,  /* a pointer or leading dimension is misaligned        */
   MM_ERR_FORMAT = 5, /* unknown element format, or a and w formats differ   */
-  MM_ERR_DEVICE = 6  /* the HIP runtime reported an error at launch         */
+  MM_ERR_DEVICE = 6, /* the HIP runtime reported an error at launch         */
+  MM_ERR_WORKSPACE = 7 /* mm_calibrate: workspace smaller than required     */
 } mm_status;
 
 typedef struct {
@@ -184,6 +188,50 @@ mm_status mm_quantize_weight(const void* w_bf16, int64_t ldw, const int32_t* per
  * MM_ERR_DEVICE.
  */
 mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, int64_t ldy, void* stream);
+
+/*
+ * Device workspace mm_calibrate needs for `rows` calibration rows of K
+ * channels: a 2048-byte block, then (chunks + 1) * K doubles and
+ * ceil(K / 256) * K int32 words, where the number of row chunks (1 .. 128)
+ * depends on rows and K only.  Host-only arithmetic.  Errors: MM_ERR_NULL (bytes is NULL),
+ * MM_ERR_SHAPE.
+ */
+mm_status mm_calibrate_workspace_size(int64_t rows, int64_t K, int64_t* bytes);
+
+/*
+ * Offline channel assignment (Sec. 3.1 "Offline channel assignment strategy";
+ * Def. 1, eq. quantization-threshold; Appendix C.2 "Derivations").  From calibration
+ * activations X [rows, K]:
+ *   M_j    = (1/rows) sum_i |X[i, j]|, summed in fp64 (exact per term) in
+ *            a fixed order for a given (rows, K), so results repeat;
+ *   sigma  = the channels sorted by ascending M, equal means in increasing
+ *            channel order (sigma[i] is the channel at sorted position i);
+ *   T(n)   = 2^b * 2^(n-1) / q_max * max|X| / 254, max over the whole of X:
+ *            T(4) with E2M1 (b 1, q_max 6), T(6) with the 6-bit format of
+ *            `formats` (E3M2: b 3, q_max 28; E2M3: b 1, q_max 7.5);
+ *   n4     = #{j : M_j <= T(4)}, n6 = #{j : T(4) < M_j <= T(6)};
+ *   split  = (p4, p6, p8) with p4 = 32 floor(n4 / 32),
+ *            p4 + p6 = 32 floor((n4 + n6) / 32), p8 = K - p4 - p6.
+ * Since the groups use the same statistic sigma sorts by, G4 = sigma[0, p4),
+ * G6 = sigma[p4, p4+p6), G8 = the rest, ready for mm_quantize_act.
+ *   x_bf16     device, bf16 [rows, K] row-major, row stride ldx elements
+ *              (ldx >= K, ldx % 8 == 0, 16-byte aligned).
+ *   formats    fp6 picks T(6)'s constants; fp8 is only validated.
+ *   workspace  device, caller-owned, 16-byte aligned, at least
+ *              mm_calibrate_workspace_size() bytes; its contents on entry are
+ *              ignored and on exit unspecified.  Calls that overlap in time
+ *              must not share it.
+ *   perm_out   device, int32 [K], 16-byte aligned: sigma.
+ *   split_out  device, int32 [3]: (p4, p6, p8); (-1, -1, -1) when X holds an
+ *              Inf or NaN, and then perm_out is the identity.
+ * Like every call it only enqueues work on `stream` (four launches); read
+ * split_out after the stream has reached it.  rows >= 1, K a positive
+ * multiple of 32, at most 32768.  Errors: MM_ERR_NULL, MM_ERR_SHAPE,
+ * MM_ERR_ALIGN, MM_ERR_FORMAT, MM_ERR_WORKSPACE, MM_ERR_DEVICE.
+ */
+mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats,
+                       void* workspace, int64_t workspace_bytes, int32_t* perm_out, int32_t* split_out,
+                       void* stream);
 
 /* Static English name of a status code. */
 const char* mm_status_str(mm_status s);

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libmicromix.so")
 
 MM_OK = 0
 STATUS_NAMES = {0: "MM_OK", 1: "MM_ERR_NULL", 2: "MM_ERR_SHAPE", 3: "MM_ERR_SPLIT", 4: "MM_ERR_ALIGN",
-                5: "MM_ERR_FORMAT", 6: "MM_ERR_DEVICE"}
+                5: "MM_ERR_FORMAT", 6: "MM_ERR_DEVICE", 7: "MM_ERR_WORKSPACE"}
 
 
 class MMSplit(ctypes.Structure):
@@ -72,6 +72,10 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mm_abi_version.restype = ctypes.c_int
     lib.mm_mx_layout_sizes.argtypes = [I64, I64, MMSplit, ctypes.POINTER(MMSizes)]
     lib.mm_mx_layout_sizes.restype = ctypes.c_int
+    lib.mm_calibrate_workspace_size.argtypes = [I64, I64, ctypes.POINTER(I64)]
+    lib.mm_calibrate_workspace_size.restype = ctypes.c_int
+    lib.mm_calibrate.argtypes = [P, I64, I64, I64, MMFormats, P, I64, P, P, P]
+    lib.mm_calibrate.restype = ctypes.c_int
     return lib
 
 
@@ -189,3 +193,41 @@ def gemm(a: MXTensor, w: MXTensor, y: torch.Tensor | None = None, stream=None) -
     _check(lib.mm_gemm(ctypes.byref(da), ctypes.byref(dw), ctypes.c_void_p(y.data_ptr()), y.stride(0),
                        _stream_ptr(stream)))
     return y
+
+
+def calibrate_workspace_size(rows: int, K: int) -> int:
+    """mm_calibrate_workspace_size: device bytes mm_calibrate needs."""
+    n = ctypes.c_int64()
+    _check(lib.mm_calibrate_workspace_size(rows, K, ctypes.byref(n)))
+    return n.value
+
+
+def calibrate_async(x: torch.Tensor, formats=DEFAULT_FORMATS, workspace: torch.Tensor | None = None,
+                    perm: torch.Tensor | None = None, split: torch.Tensor | None = None, stream=None):
+    """mm_calibrate: enqueue the offline channel assignment of bf16 calibration
+    activations x [L, K]; returns the device tensors (perm int32 [K],
+    split int32 [3]) it writes."""
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bfloat16 tensor")
+    rows, K = x.shape
+    if workspace is None:
+        workspace = torch.empty(calibrate_workspace_size(rows, K), dtype=torch.uint8, device=x.device)
+    if perm is None:
+        perm = torch.empty(K, dtype=torch.int32, device=x.device)
+    if split is None:
+        split = torch.empty(3, dtype=torch.int32, device=x.device)
+    fm = MMFormats(FP6_FORMATS.get(formats[0], -1), FP8_FORMATS.get(formats[1], -1))
+    _check(lib.mm_calibrate(ctypes.c_void_p(x.data_ptr()), rows, K, x.stride(0), fm,
+                            ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                            ctypes.c_void_p(perm.data_ptr()), ctypes.c_void_p(split.data_ptr()), _stream_ptr(stream)))
+    return perm, split
+
+
+def calibrate(x: torch.Tensor, formats=DEFAULT_FORMATS, stream=None):
+    """mm_calibrate, then wait for it: (sigma as a device int32 tensor, split
+    as a host tuple).  Raises ValueError if x holds Inf or NaN."""
+    perm, split = calibrate_async(x, formats, stream=stream)
+    p = tuple(int(v) for v in split.cpu().tolist())
+    if p[0] < 0:
+        raise ValueError("calibration input holds Inf or NaN")
+    return perm, p

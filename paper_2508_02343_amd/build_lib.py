@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmicromix.so")
-SOURCES = ["api.cpp", "quantize.hip", "gemm_direct.hip", "gemm_tiled.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "gemm_direct.hip", "gemm_tiled.hip", "calibrate.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

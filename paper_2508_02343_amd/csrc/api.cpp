@@ -17,6 +17,10 @@ constexpr int64_t kMaxRows = (int64_t)1 << 31;
 // Up to this many activation rows the GEMM streams operands straight from
 // global memory (memory-bound decode); above it the LDS-tiled kernel runs.
 constexpr int64_t kDirectMaxM = 64;
+// Calibration workspace: the workgroup maxima (nchunks * tiles <= 256 words)
+// and the per-block group counts (2 * K / 256 <= 256 words), then fp64
+// partial sums and means, then int32 per-slice rank counts.
+constexpr int64_t kCalibHeaderBytes = 2048;
 
 thread_local char g_err[512];
 
@@ -118,6 +122,40 @@ mm_status quantize(const void* x, int64_t ldx, const int32_t* perm, const mm_mx_
   return MM_OK;
 }
 
+// Row chunks of the calibration column sums: at most one workgroup per CU
+// over the 512-channel tiles (more concurrent row streams lose DRAM
+// locality), 1 .. 128 chunks, at least 64 rows per chunk.  Depends only on
+// (rows, K), so results are reproducible.
+struct CalibPlan {
+  int nchunks;
+  int tiles;
+  int64_t chunk_rows;
+  int64_t bytes;  // workspace
+};
+
+CalibPlan calib_plan(int64_t rows, int64_t K) {
+  CalibPlan p;
+  p.tiles = (int)((K + 511) / 512);
+  int64_t n = mm::kCalibMaxWorkgroups / p.tiles;
+  n = n < 1 ? 1 : (n > 128 ? 128 : n);
+  const int64_t max_n = (rows + 63) / 64;
+  if (n > max_n) n = max_n;
+  p.chunk_rows = (rows + n - 1) / n;
+  p.nchunks = (int)((rows + p.chunk_rows - 1) / p.chunk_rows);
+  const int64_t nslices = (K + mm::kCalibSlice - 1) / mm::kCalibSlice;
+  p.bytes = kCalibHeaderBytes + ((int64_t)p.nchunks + 1) * K * (int64_t)sizeof(double) +
+            nslices * K * (int64_t)sizeof(int32_t);
+  return p;
+}
+
+mm_status check_calib_shape(int64_t rows, int64_t K, const char* who) {
+  if (rows <= 0 || rows >= kMaxRows) return fail(MM_ERR_SHAPE, "%s: rows=%lld out of range", who, (long long)rows);
+  if (K <= 0 || K % 32 != 0 || K > kMaxQuantK)
+    return fail(MM_ERR_SHAPE, "%s: K=%lld must be a positive multiple of 32, at most %lld", who, (long long)K,
+                (long long)kMaxQuantK);
+  return MM_OK;
+}
+
 mm::Operand operand(const mm_mx_tensor* t) {
   mm::Operand o;
   o.q[0] = t->q4;
@@ -170,6 +208,57 @@ mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, in
   return MM_OK;
 }
 
+mm_status mm_calibrate_workspace_size(int64_t rows, int64_t K, int64_t* bytes) {
+  g_err[0] = 0;
+  if (!bytes) return fail(MM_ERR_NULL, "mm_calibrate_workspace_size: bytes is NULL");
+  mm_status st = check_calib_shape(rows, K, "mm_calibrate_workspace_size");
+  if (st != MM_OK) return st;
+  *bytes = calib_plan(rows, K).bytes;
+  return MM_OK;
+}
+
+mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats, void* workspace,
+                       int64_t workspace_bytes, int32_t* perm_out, int32_t* split_out, void* stream) {
+  g_err[0] = 0;
+  const char* who = "mm_calibrate";
+  if (!x_bf16 || !workspace || !perm_out || !split_out) return fail(MM_ERR_NULL, "%s: a pointer is NULL", who);
+  mm_status st = check_calib_shape(rows, K, who);
+  if (st != MM_OK) return st;
+  if (ldx < K) return fail(MM_ERR_SHAPE, "%s: ld=%lld below K=%lld", who, (long long)ldx, (long long)K);
+  if ((formats.fp6 != MM_FP6_E3M2 && formats.fp6 != MM_FP6_E2M3) ||
+      (formats.fp8 != MM_FP8_E4M3 && formats.fp8 != MM_FP8_E5M2))
+    return fail(MM_ERR_FORMAT, "%s: unknown element format (fp6=%d, fp8=%d)", who, formats.fp6, formats.fp8);
+  const CalibPlan p = calib_plan(rows, K);
+  if ((int64_t)p.nchunks * p.tiles * 4 > kCalibHeaderBytes / 2 || 2 * ((K + 255) / 256) * 4 > kCalibHeaderBytes / 2)
+    return fail(MM_ERR_SHAPE, "%s: internal plan exceeds the workspace header", who);
+  if (workspace_bytes < p.bytes)
+    return fail(MM_ERR_WORKSPACE, "%s: workspace of %lld bytes, %lld needed", who, (long long)workspace_bytes,
+                (long long)p.bytes);
+  if (!aligned16(x_bf16) || ldx % 8 != 0) return fail(MM_ERR_ALIGN, "%s: input must be 16-byte aligned with ld %% 8 == 0", who);
+  if (!aligned16(workspace) || !aligned16(perm_out) || ((uintptr_t)split_out & 3u))
+    return fail(MM_ERR_ALIGN, "%s: workspace and perm must be 16-byte aligned, split 4-byte aligned", who);
+  mm::CalibArgs a;
+  a.x = static_cast<const uint16_t*>(x_bf16);
+  a.ldx = ldx;
+  a.rows = rows;
+  a.K = (int)K;
+  a.nchunks = p.nchunks;
+  a.chunk_rows = p.chunk_rows;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  a.wgmax = reinterpret_cast<uint32_t*>(ws);
+  a.nmax = p.nchunks * p.tiles;
+  a.counts = reinterpret_cast<int32_t*>(ws + kCalibHeaderBytes / 2);
+  a.partial = reinterpret_cast<double*>(ws + kCalibHeaderBytes);
+  a.mean = a.partial + (int64_t)p.nchunks * K;
+  a.slice_counts = reinterpret_cast<int32_t*>(a.mean + K);
+  a.perm = perm_out;
+  a.split = split_out;
+  a.fp6_e2m3 = formats.fp6 == MM_FP6_E2M3;
+  hipError_t e = mm::launch_calibrate(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(MM_ERR_DEVICE, "%s: launch failed: %s", who, hipGetErrorString(e));
+  return MM_OK;
+}
+
 mm_status mm_mx_layout_sizes(int64_t rows, int64_t K, mm_split split, mm_mx_sizes* out) {
   g_err[0] = 0;
   if (!out) return fail(MM_ERR_NULL, "mm_mx_layout_sizes: out is NULL");
@@ -192,6 +281,7 @@ const char* mm_status_str(mm_status s) {
     case MM_ERR_ALIGN: return "MM_ERR_ALIGN";
     case MM_ERR_FORMAT: return "MM_ERR_FORMAT";
     case MM_ERR_DEVICE: return "MM_ERR_DEVICE";
+    case MM_ERR_WORKSPACE: return "MM_ERR_WORKSPACE";
   }
   return "MM_ERR_UNKNOWN";
 }

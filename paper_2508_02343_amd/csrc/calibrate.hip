@@ -1,0 +1,231 @@
+// Offline calibration (Sec. 3.1 "Offline Channel Assignment Strategy";
+// Def. 1, eq. quantization-threshold; Appendix C.2 "Derivations"): from
+// calibration activations X [L, K] compute each channel's mean |X|, the
+// stable ascending order sigma of those means, and the group sizes given by
+// the thresholds
+//   T(n) = 2^b * 2^(n-1) / q_max * max|X| / 254
+// of E2M1 (n = 4) and the 6-bit format (n = 6).  A channel belongs to G4 when
+// its mean is <= T(4), to G6 when it is <= T(6), else to G8; each count is
+// rounded down to a multiple of 32, so channels only ever move to a wider
+// group.
+//
+// Four stream-ordered launches, deterministic for a given (L, K):
+//   1. column sums: each workgroup adds |x| in fp64 over one 512-channel tile
+//      and one fixed chunk of rows (HBM-bound, 2 bytes read per element) and
+//      writes its partial sums and its largest |x|.  About one workgroup per
+//      CU streams best: more concurrent row streams lose DRAM locality;
+//   2. means: each channel adds its chunk partials in a fixed order, / L;
+//   3. rank: workgroup (jb, sl) compares 256 channels with a 256-channel
+//      slice of the means and stores, per channel, how many of them sort
+//      before it under the strict order (mean, index); the workgroups of
+//      slice 0 also evaluate the thresholds against the largest |x| and count
+//      their channels' groups;
+//   4. place: rank[j] = the sum of j's slice counts, sigma[rank[j]] = j, and
+//      workgroup 0 sums the group counts into the split.
+// No atomics: every result is written by exactly one thread.
+#include "kernels.hpp"
+
+namespace mm {
+namespace {
+
+constexpr int kSumWaves = 4;               // waves per column-sum workgroup
+constexpr int kLaneCols = 8;               // channels per lane (one 16-byte load)
+constexpr int kTileCols = 64 * kLaneCols;  // channels per column-sum workgroup
+constexpr int kMeanWaves = 16;             // waves per mean workgroup (one chunk subset each)
+constexpr int kRankThreads = 256;          // channels per rank workgroup
+constexpr int kRankSlice = kCalibSlice;    // means compared per rank workgroup
+constexpr uint32_t kF32Inf = 0x7F800000u;  // |x| fp32 patterns at or above this are Inf or NaN
+
+// |x| of the two bf16 values in a 32-bit word, as fp32 bit patterns (a bf16
+// is the top half of an fp32; clearing the sign bit gives |x|).  Their
+// conversion to fp64 is exact: the kernels keep fp32 denormals (the default
+// floating-point mode), so subnormal inputs are not flushed.
+__device__ __forceinline__ void add_word(double* s, uint32_t& mx, uint32_t w) {
+  const uint32_t lo = (w << 16) & 0x7FFF0000u, hi = w & 0x7FFF0000u;
+  s[0] += (double)__uint_as_float(lo);
+  s[1] += (double)__uint_as_float(hi);
+  mx = max(mx, max(lo, hi));
+}
+
+__device__ __forceinline__ void add_row(double* s, uint32_t& mx, uint4 v) {
+  add_word(s + 0, mx, v.x);
+  add_word(s + 2, mx, v.y);
+  add_word(s + 4, mx, v.z);
+  add_word(s + 6, mx, v.w);
+}
+
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Largest |x| of the whole input (fp32 bit pattern), from the column-sum
+// workgroups' maxima; every thread of a kRankThreads workgroup gets it.
+__device__ uint32_t input_amax(const CalibArgs& a, uint32_t* lds4) {
+  uint32_t m = 0u;
+  for (int i = threadIdx.x; i < a.nmax; i += kRankThreads) m = max(m, a.wgmax[i]);
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = m;
+  __syncthreads();
+  return max(max(lds4[0], lds4[1]), max(lds4[2], lds4[3]));
+}
+
+// How many of the n means in `tile` (channels base .. base+n-1, n a multiple
+// of 32) sort before channel j with mean mj.  MODE 0: every tile channel
+// has a larger index than j (ties do not count); MODE 1: every one has a
+// smaller index (ties count); MODE 2: the slice holds j, jl = j - base.
+template <int MODE>
+__device__ __forceinline__ int count_before(const double* tile, int n, double mj, int jl) {
+  int cnt = 0;
+  for (int i0 = 0; i0 < n; i0 += 32) {
+#pragma unroll
+    for (int k = 0; k < 32; k += 2) {
+      const double2 v = *reinterpret_cast<const double2*>(tile + i0 + k);
+      if constexpr (MODE == 0) cnt += (v.x < mj) + (v.y < mj);
+      else if constexpr (MODE == 1) cnt += (v.x <= mj) + (v.y <= mj);
+      else  // bitwise, not short-circuit: no per-lane branches
+        cnt += ((int)(v.x < mj) | ((int)(v.x == mj) & (int)(i0 + k < jl))) +
+               ((int)(v.y < mj) | ((int)(v.y == mj) & (int)(i0 + k + 1 < jl)));
+    }
+  }
+  return cnt;
+}
+
+__global__ __launch_bounds__(64 * kSumWaves) void colsum_kernel(CalibArgs a) {
+  __shared__ double red[kSumWaves - 1][kLaneCols][64];
+  __shared__ uint32_t wmax[kSumWaves];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c0 = blockIdx.x * kTileCols + lane * kLaneCols;
+  const int64_t r0 = (int64_t)blockIdx.y * a.chunk_rows;
+  const int64_t r1 = min(a.rows, r0 + a.chunk_rows);
+  double s[kLaneCols];
+  for (int i = 0; i < kLaneCols; ++i) s[i] = 0.0;
+  uint32_t mx = 0u;
+  if (c0 < a.K) {
+    // wave w adds rows r0 + w, r0 + w + 4, ... in increasing order
+    const uint16_t* p = a.x + c0;
+    int64_t r = r0 + wave;
+    constexpr int U = 8;
+    for (; r + (U - 1) * kSumWaves < r1; r += U * kSumWaves) {
+      uint4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = *reinterpret_cast<const uint4*>(p + (r + u * kSumWaves) * a.ldx);
+#pragma unroll
+      for (int u = 0; u < U; ++u) add_row(s, mx, v[u]);
+    }
+    for (; r < r1; r += kSumWaves) add_row(s, mx, *reinterpret_cast<const uint4*>(p + r * a.ldx));
+  }
+  mx = wave_max(mx);
+  if (lane == 0) wmax[wave] = mx;
+  // fixed-order combine of the four waves' partial sums
+  if (wave > 0)
+    for (int i = 0; i < kLaneCols; ++i) red[wave - 1][i][lane] = s[i];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t m = wmax[0];
+    for (int w = 1; w < kSumWaves; ++w) m = max(m, wmax[w]);
+    a.wgmax[blockIdx.y * gridDim.x + blockIdx.x] = m;
+  }
+  if (wave != 0 || c0 >= a.K) return;
+  for (int w = 0; w < kSumWaves - 1; ++w)
+    for (int i = 0; i < kLaneCols; ++i) s[i] += red[w][i][lane];
+  double2* out = reinterpret_cast<double2*>(a.partial + (int64_t)blockIdx.y * a.K + c0);
+  for (int i = 0; i < kLaneCols / 2; ++i) out[i] = make_double2(s[2 * i], s[2 * i + 1]);
+}
+
+__global__ __launch_bounds__(64 * kMeanWaves) void mean_kernel(CalibArgs a) {
+  __shared__ double red[kMeanWaves][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + lane;
+  double s = 0.0;
+  if (j < a.K)
+    for (int c = wave; c < a.nchunks; c += kMeanWaves) s += a.partial[(int64_t)c * a.K + j];
+  red[wave][lane] = s;
+  __syncthreads();
+  if (wave != 0 || j >= a.K) return;
+  for (int w = 1; w < kMeanWaves; ++w) s += red[w][lane];
+  a.mean[j] = s / (double)a.rows;
+}
+
+__global__ __launch_bounds__(kRankThreads) void rank_kernel(CalibArgs a) {
+  __shared__ __align__(16) double tile[kRankSlice];
+  __shared__ uint32_t lds4[4];
+  __shared__ int c4[4], c6[4];
+  const int jb = blockIdx.x * kRankThreads, j = jb + threadIdx.x;
+  const int base = blockIdx.y * kRankSlice;
+  const int n = min(kRankSlice, a.K - base);
+  const double mj = j < a.K ? a.mean[j] : 0.0;
+  for (int i = threadIdx.x; i < n; i += kRankThreads) tile[i] = a.mean[base + i];
+  __syncthreads();
+  int cnt;
+  if (jb + kRankThreads <= base) cnt = count_before<0>(tile, n, mj, 0);  // uniform per workgroup
+  else if (jb >= base + n) cnt = count_before<1>(tile, n, mj, 0);
+  else cnt = count_before<2>(tile, n, mj, j - base);
+  if (j < a.K) a.slice_counts[(int64_t)blockIdx.y * a.K + j] = cnt;
+  if (blockIdx.y != 0) return;
+  // group counts of this workgroup's channels (slice 0 only: once per channel)
+  const uint32_t amax = input_amax(a, lds4);
+  // thresholds, in the order of operations of their definition
+  const double tx = (double)__uint_as_float(amax);
+  const double t4 = 2.0 * 8.0 / 6.0 * (tx / 254.0);                                  // E2M1: b 1, q_max 6
+  const double t6 = a.fp6_e2m3 ? 2.0 * 32.0 / 7.5 * (tx / 254.0)                     // E2M3: b 1, q_max 7.5
+                               : 8.0 * 32.0 / 28.0 * (tx / 254.0);                   // E3M2: b 3, q_max 28
+  const bool in4 = j < a.K && mj <= t4;
+  const bool in6 = j < a.K && !in4 && mj <= t6;
+  const int n4 = wave_sum(in4), n6 = wave_sum(in6);
+  if ((threadIdx.x & 63) == 0) {
+    c4[threadIdx.x >> 6] = n4;
+    c6[threadIdx.x >> 6] = n6;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    a.counts[2 * blockIdx.x] = c4[0] + c4[1] + c4[2] + c4[3];
+    a.counts[2 * blockIdx.x + 1] = c6[0] + c6[1] + c6[2] + c6[3];
+  }
+}
+
+__global__ __launch_bounds__(kRankThreads) void place_kernel(CalibArgs a) {
+  __shared__ uint32_t lds4[4];
+  const bool finite = input_amax(a, lds4) < kF32Inf;
+  const int j = blockIdx.x * kRankThreads + threadIdx.x;
+  if (j < a.K) {
+    const int nslices = (a.K + kRankSlice - 1) / kRankSlice;
+    int rank = 0;
+#pragma unroll 8
+    for (int sl = 0; sl < nslices; ++sl) rank += a.slice_counts[(int64_t)sl * a.K + j];
+    a.perm[finite ? rank : j] = j;
+  }
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  if (!finite) {
+    a.split[0] = a.split[1] = a.split[2] = -1;
+    return;
+  }
+  int n4 = 0, n6 = 0;
+  for (int b = 0; b < (int)gridDim.x; ++b) {
+    n4 += a.counts[2 * b];
+    n6 += a.counts[2 * b + 1];
+  }
+  const int p4 = n4 / 32 * 32, p46 = (n4 + n6) / 32 * 32;
+  a.split[0] = p4;
+  a.split[1] = p46 - p4;
+  a.split[2] = a.K - p46;
+}
+
+}  // namespace
+
+hipError_t launch_calibrate(const CalibArgs& a, hipStream_t stream) {
+  const int tiles = (a.K + kTileCols - 1) / kTileCols;
+  hipLaunchKernelGGL(colsum_kernel, dim3(tiles, a.nchunks), dim3(64 * kSumWaves), 0, stream, a);
+  hipLaunchKernelGGL(mean_kernel, dim3((a.K + 63) / 64), dim3(64 * kMeanWaves), 0, stream, a);
+  hipLaunchKernelGGL(rank_kernel, dim3((a.K + kRankThreads - 1) / kRankThreads, (a.K + kRankSlice - 1) / kRankSlice),
+                     dim3(kRankThreads), 0, stream, a);
+  hipLaunchKernelGGL(place_kernel, dim3((a.K + kRankThreads - 1) / kRankThreads), dim3(kRankThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mm

@@ -59,7 +59,30 @@ struct GemmArgs {
   int fs;  // format set of both operands (as QuantArgs::fs)
 };
 
+// Offline calibration over X [rows, K]: channel sums in fixed row chunks,
+// means, the stable order of the means, and the split.
+constexpr int kCalibMaxWorkgroups = 256;  // column-sum workgroups at most (one per CU)
+constexpr int kCalibSlice = 256;          // means per rank slice
+struct CalibArgs {
+  const uint16_t* x;
+  int64_t ldx;  // elements
+  int64_t rows;
+  int K;
+  int nchunks;         // row chunks of the column sums
+  int64_t chunk_rows;  // rows per chunk (the last may be shorter)
+  uint32_t* wgmax;     // [nmax] largest |x| of each column-sum workgroup, fp32 bit patterns
+  int nmax;            // nchunks * tiles
+  double* partial;     // [nchunks, K] per-chunk sums of |x|
+  double* mean;        // [K]
+  int32_t* slice_counts;  // [ceil(K / 256), K] channels of each 256-slice that sort before j
+  int32_t* counts;     // [2 * ceil(K / 256)] G4 and G6 counts per 256-channel block
+  int32_t* perm;       // [K] output sigma
+  int32_t* split;      // [3] output (p4, p6, p8)
+  int fp6_e2m3;        // T(6) with E2M3's constants instead of E3M2's
+};
+
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream);
+hipError_t launch_calibrate(const CalibArgs& a, hipStream_t stream);
 hipError_t launch_gemm_direct(const GemmArgs& a, hipStream_t stream);
 hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t stream);
 

@@ -23,10 +23,10 @@ def _declared_functions():
     return sorted(set(re.findall(r"\b(mm_[a-z_]+)\s*\(", text)))
 
 
-def test_header_declares_the_three_calls():
+def test_header_declares_the_calls():
     names = _declared_functions()
-    for n in ("mm_quantize_act", "mm_quantize_weight", "mm_gemm", "mm_status_str", "mm_last_error",
-              "mm_abi_version"):
+    for n in ("mm_quantize_act", "mm_quantize_weight", "mm_gemm", "mm_calibrate", "mm_calibrate_workspace_size",
+              "mm_status_str", "mm_last_error", "mm_abi_version"):
         assert n in names
 
 
@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(b.LIB_PATH)
     for n in _declared_functions():
         assert hasattr(lib, n), n
-    assert b.lib.mm_abi_version() == 3
+    assert b.lib.mm_abi_version() == 4
 
 
 def test_status_strings():
@@ -180,3 +180,57 @@ def test_gemm_rejects_mixed_formats():
     w.formats = b.MMFormats(1, 0)
     st = b.lib.mm_gemm(ctypes.byref(a), ctypes.byref(w), ctypes.c_void_p(FAKE), 128, None)
     assert b.STATUS_NAMES[st] == "MM_ERR_FORMAT"
+
+
+def _ws(rows, K):
+    n = ctypes.c_int64(-1)
+    st = b.lib.mm_calibrate_workspace_size(rows, K, ctypes.byref(n))
+    return b.STATUS_NAMES[st], n.value
+
+
+@pytest.mark.parametrize("rows,K", [(1, 32), (16, 32), (17, 4096), (2048, 4096), (4096, 14336), (8192, 32768),
+                                    (100000, 512)])
+def test_calibrate_workspace_size(rows, K):
+    st, n = _ws(rows, K)
+    assert st == "MM_OK"
+    doubles, rem = divmod(n - 2048 - 4 * K * -(-K // 256), 8 * K)  # (chunks + 1) * K doubles: partial sums and means
+    chunks = doubles - 1
+    assert rem == 0 and 1 <= chunks <= 128
+    assert chunks - 1 <= (rows - 1) // 64  # at least 64 rows per chunk, except a single chunk
+    if rows == 1:
+        assert chunks == 1
+
+
+def test_calibrate_workspace_size_rejects():
+    assert _ws(0, 64)[0] == "MM_ERR_SHAPE"
+    assert _ws(4, 100)[0] == "MM_ERR_SHAPE"
+    assert _ws(4, 65536)[0] == "MM_ERR_SHAPE"
+    assert b.STATUS_NAMES[b.lib.mm_calibrate_workspace_size(4, 64, None)] == "MM_ERR_NULL"
+
+
+def _cal(rows=64, K=128, ldx=None, fm=(0, 0), x=FAKE, ws=FAKE, wsb=None, perm=FAKE, split=FAKE):
+    if wsb is None:
+        wsb = _ws(rows, K)[1] if _ws(rows, K)[0] == "MM_OK" else 1 << 30
+    st = b.lib.mm_calibrate(ctypes.c_void_p(x), rows, K, ldx if ldx is not None else K, b.MMFormats(*fm),
+                            ctypes.c_void_p(ws), wsb, ctypes.c_void_p(perm), ctypes.c_void_p(split), None)
+    return b.STATUS_NAMES[st]
+
+
+def test_calibrate_rejects_bad_arguments():
+    assert _cal(x=0) == "MM_ERR_NULL"
+    assert _cal(ws=0) == "MM_ERR_NULL"
+    assert _cal(perm=0) == "MM_ERR_NULL"
+    assert _cal(split=0) == "MM_ERR_NULL"
+    assert _cal(rows=0) == "MM_ERR_SHAPE"
+    assert _cal(K=96 + 8) == "MM_ERR_SHAPE"
+    assert _cal(K=65536) == "MM_ERR_SHAPE"
+    assert _cal(ldx=96) == "MM_ERR_SHAPE"
+    assert _cal(fm=(2, 0)) == "MM_ERR_FORMAT"
+    assert _cal(fm=(0, 5)) == "MM_ERR_FORMAT"
+    assert _cal(wsb=_ws(64, 128)[1] - 8) == "MM_ERR_WORKSPACE"
+    assert _cal(x=FAKE + 2) == "MM_ERR_ALIGN"
+    assert _cal(ldx=132) == "MM_ERR_ALIGN"
+    assert _cal(ws=FAKE + 8) == "MM_ERR_ALIGN"
+    assert _cal(perm=FAKE + 4) == "MM_ERR_ALIGN"
+    assert _cal(split=FAKE + 2) == "MM_ERR_ALIGN"
+    assert b.lib.mm_last_error().decode()

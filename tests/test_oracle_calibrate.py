@@ -11,6 +11,7 @@ import pytest
 
 from oracle import mx_oracle as O
 from paper_2508_02343_amd import workloads as W
+from tests.calib_cases import boundary_case
 
 
 def test_thresholds_closed_form():
@@ -104,3 +105,29 @@ def test_e2m3_threshold_uses_its_own_constants():
     x[0, 95] = 254.0  # t = 254: T(4) = 8/3, T(6) = 64/7 ~ 9.14 (E3M2) or 8.53 (E2M3)
     assert O.calibrate(_bits(x))[1] == (32, 32, 32)
     assert O.calibrate(_bits(x), (O.E2M1, O.E2M3, O.E4M3))[1] == (32, 0, 64)
+
+
+def test_means_exactly_at_the_thresholds_take_the_narrower_group():
+    x = boundary_case()
+    M = O.channel_abs_mean(_bits(x))
+    assert M[31] == O.quantization_threshold(O.E2M1, 254.0) == 8 / 3
+    assert M[63] == O.quantization_threshold(O.E3M2, 254.0) == 64 / 7
+    assert O.calibrate(_bits(x))[1] == (32, 32, 32)
+    # nudging either boundary channel up by one bf16 step moves the block boundary
+    y = x.copy()
+    y[20, 31] = 16.125
+    assert O.calibrate(_bits(y))[1] == (0, 64, 32)
+    y = x.copy()
+    y[20, 63] = 32.25
+    assert O.calibrate(_bits(y))[1] == (32, 0, 64)
+
+
+def test_subnormal_channels_are_not_flushed():
+    from tests.calib_cases import subnormal_case
+
+    bits = subnormal_case()
+    M = O.channel_abs_mean(bits)
+    assert M[5] == 2.0 ** -133 and M[9] == 2.0 ** -126
+    sigma, split = O.calibrate(bits)
+    assert list(sigma) == [j for j in range(32) if j not in (5, 9)] + [5, 9]
+    assert split == (0, 0, 32)  # 31 channels at or below T(4): rounds down to 0
