@@ -145,7 +145,7 @@ def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps
     ms = e0.elapsed_time(e1) / reps
     nbytes = rows * w.K * 2 + w.K * 4 + 12
     gbps = nbytes / (ms * 1e-3) / 1e9
-    return {"kernel": "offline calibration (mm_calibrate, 5 launches)", "rows": rows, "K": w.K, "ms": round(ms, 5),
+    return {"kernel": "offline calibration (mm_calibrate, 4 launches)", "rows": rows, "K": w.K, "ms": round(ms, 5),
             "achieved": round(gbps, 1), "peak": PEAK_HBM, "unit": "GB/s", "frac": round(gbps / PEAK_HBM, 4),
             "bytes_per_call": nbytes, "split": split.cpu().tolist()}
 
