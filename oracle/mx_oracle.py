@@ -52,6 +52,12 @@ R13 calibration: a channel's statistic against the thresholds T(4), T(6) is
     taken over the whole calibration tensor; the counts are rounded down to
     multiples of 32 (channels move to the next wider group, never to a
     narrower one); T(6) uses the constants of the MXFP6 variant in use.
+R14 the normalisation fused with the reorder-and-quantize is RMSNorm (the
+    norm of the Llama and Qwen models the paper evaluates), evaluated as bf16
+    frameworks do: the row factor r = 1/sqrt(mean(x^2) + eps) in float64,
+    rounded once to fp32; x * r as an fp32 product rounded to bf16; that
+    times the bf16 weight gamma as an fp32 product rounded to bf16 again.
+    The quantiser then sees these bf16 values.
 """
 
 from __future__ import annotations
@@ -484,3 +490,35 @@ def calibrate(x_bf16_bits: np.ndarray, formats=PARTITION_FORMATS):
     p4 = n4 // BLOCK * BLOCK
     p46 = (n4 + n6) // BLOCK * BLOCK
     return sigma, (p4, p46 - p4, K - p46)
+
+
+# ---------------------------------------------------------------------------
+# RMSNorm fused before the reorder-and-quantize (App. D.2, Fig.
+# "precision-mapping": the reorder-and-quantize runs inside the layer's
+# normalisation; reading R14)
+# ---------------------------------------------------------------------------
+
+
+def rmsnorm_bf16(x_bf16_bits: np.ndarray, gamma_bf16_bits: np.ndarray, eps: float) -> np.ndarray:
+    """bf16 bit patterns of RMSNorm(X)[i, j] = gamma_j * X_ij / sqrt(mean_j X_ij^2 + eps),
+    with the roundings of reading R14."""
+    x = bf16_bits_to_f64(np.asarray(x_bf16_bits, dtype=np.uint16))
+    g = bf16_bits_to_f64(np.asarray(gamma_bf16_bits, dtype=np.uint16))
+    if x.ndim != 2 or g.shape != (x.shape[1],):
+        raise ValueError("X must be [L, K] and gamma [K]")
+    K = x.shape[1]
+    ms = (x * x).sum(axis=1) / K  # every square of a bf16 value is exact in float64
+    r = 1.0 / np.sqrt(ms + float(np.float32(eps)))
+    r32 = r.astype(np.float32)  # one rounding, to nearest even
+    t = x.astype(np.float32) * r32[:, None]  # fp32 products (exact inputs), rounded to nearest even
+    y1 = f64_to_bf16_bits(t.astype(np.float64))
+    u = bf16_bits_to_f64(y1).astype(np.float32) * g.astype(np.float32)[None, :]
+    return f64_to_bf16_bits(u.astype(np.float64))
+
+
+def rmsnorm_row_factor(x_bf16_bits: np.ndarray, eps: float) -> np.ndarray:
+    """The float64 row factors r = 1/sqrt(mean(x^2) + eps) before their
+    rounding to fp32 (for checks of how close a row sits to a rounding
+    boundary)."""
+    x = bf16_bits_to_f64(np.asarray(x_bf16_bits, dtype=np.uint16))
+    return 1.0 / np.sqrt((x * x).sum(axis=1) / x.shape[1] + float(np.float32(eps)))
