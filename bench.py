@@ -239,6 +239,11 @@ def main() -> int:
     quant_ms = timed(lambda i: B.quantize_act(X[i % nbuf], perm, w.split, out=XQ[i % nbuf], stream=stream),
                      args.steps)
     gemm_ms = timed(lambda i: B.gemm(XQ[i % nbuf], WQ[i % nbuf], y=Y[i % nbuf], stream=stream), args.steps)
+    # the same quantiser with the layer's RMSNorm fused in front (weight ~ 1 + N(0, 0.25^2), eps 1e-5)
+    g_np = (1.0 + 0.25 * np.random.default_rng([w.seed, 9]).standard_normal(w.K)).astype(np.float32)
+    gamma = to_bf16(W.f32_to_bf16_bits(g_np))
+    norm_ms = timed(lambda i: B.rmsnorm_quantize_act(X[i % nbuf], gamma, 1e-5, perm, w.split, out=XQ[i % nbuf],
+                                                     stream=stream), args.steps)
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     flops = 2.0 * w.M * w.N * w.K
@@ -277,6 +282,10 @@ def main() -> int:
         "quantizer": {"kernel": "reorder-and-quantize (activation)", "ms": round(quant_ms, 5),
                       "achieved": round(quant_gbps, 1), "peak": PEAK_HBM, "unit": "GB/s",
                       "frac": round(quant_gbps / PEAK_HBM, 4), "bytes_per_launch": qbytes},
+        "rmsnorm_quantizer": {"kernel": "RMSNorm fused with reorder-and-quantize", "ms": round(norm_ms, 5),
+                              "achieved": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM,
+                              "unit": "GB/s", "frac": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
+                              "vs_plain_quantizer": round(norm_ms / quant_ms, 3)},
         "gemm_ms": round(gemm_ms, 5),
         "quant_share_of_kernel_time": round(quant_ms / (quant_ms + gemm_ms), 4),
         "weight_quantize": {"ms": round(wq_ms, 5), "GB/s": round(wq_gbps, 1)},

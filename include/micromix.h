@@ -13,9 +13,11 @@
  * sums all three partitions in fp32 and writes bfloat16 (Sec. 2.1 eq. 1;
  * Sec. 3.2 "GEMM kernel").
  *
- * Three calls implement that path, and a fourth prepares it offline:
+ * These calls implement that path, and mm_calibrate prepares it offline:
  *   mm_quantize_act     online fused reorder-and-quantize of activations
  *                       (Sec. 3.2 "Quantization kernel", Fig. "micromix-design" b)
+ *   mm_rmsnorm_quantize_act  the same, with the layer's RMSNorm fused in
+ *                       front (App. D.2, Fig. "precision-mapping")
  *   mm_quantize_weight  the same transform for weights, run once offline
  *                       with the activation's sigma and split (Sec. 3.2)
  *   mm_gemm             mixed-precision block-scaled GEMM, Y = A W^T
@@ -94,7 +96,7 @@
 extern "C" {
 #endif
 
-#define MM_ABI_VERSION 4
+#define MM_ABI_VERSION 5
 
 typedef enum {
   MM_OK = 0,
@@ -104,7 +106,8 @@ typedef enum {
   MM_ERR_ALIGN = 4,  /* a pointer or leading dimension is misaligned        */
   MM_ERR_FORMAT = 5, /* unknown element format, or a and w formats differ   */
   MM_ERR_DEVICE = 6, /* the HIP runtime reported an error at launch         */
-  MM_ERR_WORKSPACE = 7 /* mm_calibrate: workspace smaller than required     */
+  MM_ERR_WORKSPACE = 7, /* mm_calibrate: workspace smaller than required    */
+  MM_ERR_VALUE = 8      /* a scalar argument out of range (eps)              */
 } mm_status;
 
 typedef struct {
@@ -163,6 +166,24 @@ mm_status mm_mx_layout_sizes(int64_t rows, int64_t K, mm_split split, mm_mx_size
  */
 mm_status mm_quantize_act(const void* x_bf16, int64_t ldx, const int32_t* perm, const mm_mx_tensor* out,
                           void* stream);
+
+/*
+ * RMSNorm fused with the reorder-and-quantize of activations (App. D.2,
+ * Fig. "precision-mapping": the reorder-and-quantize runs inside the layer's
+ * normalisation, so the normalised bf16 activation never goes to memory).
+ * Each row x is replaced by
+ *   y_j = bf16( gamma_j * bf16( x_j * r ) ),  r = fp32( 1 / sqrt(mean_j x_j^2 + eps) )
+ * (r evaluated in fp64 and rounded once to fp32; both products in fp32,
+ * each rounded to nearest even), and y is quantised exactly as
+ * mm_quantize_act would quantise it.
+ *   gamma_bf16  device, bf16 [K] in the original channel order (2-byte
+ *               aligned, finite).
+ *   eps         finite and > 0 (MM_ERR_VALUE otherwise).
+ * The other arguments, the layout and the errors are those of
+ * mm_quantize_act (plus MM_ERR_VALUE; MM_ERR_NULL for a NULL gamma).
+ */
+mm_status mm_rmsnorm_quantize_act(const void* x_bf16, int64_t ldx, const void* gamma_bf16, float eps,
+                                  const int32_t* perm, const mm_mx_tensor* out, void* stream);
 
 /*
  * Offline reorder-and-quantize of a weight W [N, K] with the sigma and split

@@ -502,23 +502,29 @@ def calibrate(x_bf16_bits: np.ndarray, formats=PARTITION_FORMATS):
 def rmsnorm_bf16(x_bf16_bits: np.ndarray, gamma_bf16_bits: np.ndarray, eps: float) -> np.ndarray:
     """bf16 bit patterns of RMSNorm(X)[i, j] = gamma_j * X_ij / sqrt(mean_j X_ij^2 + eps),
     with the roundings of reading R14."""
-    x = bf16_bits_to_f64(np.asarray(x_bf16_bits, dtype=np.uint16))
-    g = bf16_bits_to_f64(np.asarray(gamma_bf16_bits, dtype=np.uint16))
-    if x.ndim != 2 or g.shape != (x.shape[1],):
-        raise ValueError("X must be [L, K] and gamma [K]")
-    K = x.shape[1]
-    ms = (x * x).sum(axis=1) / K  # every square of a bf16 value is exact in float64
-    r = 1.0 / np.sqrt(ms + float(np.float32(eps)))
-    r32 = r.astype(np.float32)  # one rounding, to nearest even
-    t = x.astype(np.float32) * r32[:, None]  # fp32 products (exact inputs), rounded to nearest even
-    y1 = f64_to_bf16_bits(t.astype(np.float64))
-    u = bf16_bits_to_f64(y1).astype(np.float32) * g.astype(np.float32)[None, :]
-    return f64_to_bf16_bits(u.astype(np.float64))
+    r32 = rmsnorm_row_factor(x_bf16_bits, eps).astype(np.float32)  # one rounding, to nearest even
+    return rmsnorm_apply(x_bf16_bits, gamma_bf16_bits, r32)
 
 
 def rmsnorm_row_factor(x_bf16_bits: np.ndarray, eps: float) -> np.ndarray:
-    """The float64 row factors r = 1/sqrt(mean(x^2) + eps) before their
-    rounding to fp32 (for checks of how close a row sits to a rounding
-    boundary)."""
+    """The float64 row factors r = 1/sqrt(mean(x^2) + eps), before their
+    rounding to fp32."""
     x = bf16_bits_to_f64(np.asarray(x_bf16_bits, dtype=np.uint16))
-    return 1.0 / np.sqrt((x * x).sum(axis=1) / x.shape[1] + float(np.float32(eps)))
+    if x.ndim != 2:
+        raise ValueError("X must be [L, K]")
+    ms = (x * x).sum(axis=1) / x.shape[1]  # every square of a bf16 value is exact in float64
+    return 1.0 / np.sqrt(ms + float(np.float32(eps)))
+
+
+def rmsnorm_apply(x_bf16_bits: np.ndarray, gamma_bf16_bits: np.ndarray, r32: np.ndarray) -> np.ndarray:
+    """bf16(gamma_j * bf16(x_ij * r_i)) for given fp32 row factors r: both
+    products in fp32 (exact inputs), each rounded to nearest even."""
+    x = bf16_bits_to_f64(np.asarray(x_bf16_bits, dtype=np.uint16))
+    g = bf16_bits_to_f64(np.asarray(gamma_bf16_bits, dtype=np.uint16))
+    r32 = np.asarray(r32, dtype=np.float32)
+    if x.ndim != 2 or g.shape != (x.shape[1],) or r32.shape != (x.shape[0],):
+        raise ValueError("X must be [L, K], gamma [K] and r [L]")
+    t = x.astype(np.float32) * r32[:, None]
+    y1 = f64_to_bf16_bits(t.astype(np.float64))
+    u = bf16_bits_to_f64(y1).astype(np.float32) * g.astype(np.float32)[None, :]
+    return f64_to_bf16_bits(u.astype(np.float64))

@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libmicromix.so")
 
 MM_OK = 0
 STATUS_NAMES = {0: "MM_OK", 1: "MM_ERR_NULL", 2: "MM_ERR_SHAPE", 3: "MM_ERR_SPLIT", 4: "MM_ERR_ALIGN",
-                5: "MM_ERR_FORMAT", 6: "MM_ERR_DEVICE", 7: "MM_ERR_WORKSPACE"}
+                5: "MM_ERR_FORMAT", 6: "MM_ERR_DEVICE", 7: "MM_ERR_WORKSPACE",
+                8: "MM_ERR_VALUE"}
 
 
 class MMSplit(ctypes.Structure):
@@ -62,7 +63,8 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mm_quantize_act.argtypes = [P, I64, P, T, P]
     lib.mm_quantize_weight.argtypes = [P, I64, P, T, P]
     lib.mm_gemm.argtypes = [T, T, P, I64, P]
-    for f in (lib.mm_quantize_act, lib.mm_quantize_weight, lib.mm_gemm):
+    lib.mm_rmsnorm_quantize_act.argtypes = [P, I64, P, ctypes.c_float, P, T, P]
+    for f in (lib.mm_quantize_act, lib.mm_quantize_weight, lib.mm_gemm, lib.mm_rmsnorm_quantize_act):
         f.restype = ctypes.c_int
     lib.mm_status_str.argtypes = [ctypes.c_int]
     lib.mm_status_str.restype = ctypes.c_char_p
@@ -175,6 +177,20 @@ def quantize_act(x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | Non
     """mm_quantize_act: fused reorder-and-quantize of bf16 activations
     (formats: of the 6-bit and 8-bit groups, used when out is None)."""
     return _quantize(lib.mm_quantize_act, x, perm, split, out, stream, formats)
+
+
+def rmsnorm_quantize_act(x: torch.Tensor, gamma: torch.Tensor, eps: float, perm: torch.Tensor, split,
+                         out: MXTensor | None = None, stream=None, formats=DEFAULT_FORMATS) -> MXTensor:
+    """mm_rmsnorm_quantize_act: RMSNorm (bf16 weight gamma [K], eps) fused
+    with the reorder-and-quantize of bf16 activations."""
+    if gamma.dtype != torch.bfloat16 or gamma.dim() != 1 or not gamma.is_contiguous() or gamma.numel() != x.shape[-1]:
+        raise ValueError("gamma must be a contiguous bfloat16 tensor [K]")
+    g = ctypes.c_void_p(gamma.data_ptr())
+
+    def fn(xp, ld, pp, d, st):
+        return lib.mm_rmsnorm_quantize_act(xp, ld, g, ctypes.c_float(eps), pp, d, st)
+
+    return _quantize(fn, x, perm, split, out, stream, formats)
 
 
 def quantize_weight(w: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None = None,

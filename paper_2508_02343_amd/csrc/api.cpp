@@ -90,16 +90,20 @@ mm_status check_tensor(const mm_mx_tensor* t, const char* name) {
 }
 
 mm_status quantize(const void* x, int64_t ldx, const int32_t* perm, const mm_mx_tensor* out, void* stream,
-                   const char* who) {
+                   const char* who, const void* gamma = nullptr, float eps = 0.0f) {
   g_err[0] = 0;
   if (!x) return fail(MM_ERR_NULL, "%s: input pointer is NULL", who);
   if (!perm) return fail(MM_ERR_NULL, "%s: perm is NULL", who);
+  const bool norm = gamma != nullptr;
   mm_status st = check_tensor(out, "out");
   if (st != MM_OK) return st;
   if (out->K > kMaxQuantK) return fail(MM_ERR_SHAPE, "%s: K=%lld exceeds %lld", who, (long long)out->K, (long long)kMaxQuantK);
   if (ldx < out->K) return fail(MM_ERR_SHAPE, "%s: ld=%lld below K=%lld", who, (long long)ldx, (long long)out->K);
   if (!aligned16(x) || ldx % 8 != 0) return fail(MM_ERR_ALIGN, "%s: input must be 16-byte aligned with ld %% 8 == 0", who);
   if (!aligned16(perm)) return fail(MM_ERR_ALIGN, "%s: perm must be 16-byte aligned", who);
+  if (norm && !(eps > 0.0f && eps <= 3.0e38f))
+    return fail(MM_ERR_VALUE, "%s: eps=%g must be finite and positive", who, (double)eps);
+  if (norm && ((uintptr_t)gamma & 1u)) return fail(MM_ERR_ALIGN, "%s: gamma must be 2-byte aligned", who);
   const Layout l = layout(out->rows, out->split);
   mm::QuantArgs a;
   a.x = static_cast<const uint16_t*>(x);
@@ -117,6 +121,9 @@ mm_status quantize(const void* x, int64_t ldx, const int32_t* perm, const mm_mx_
   a.q[2] = out->q8;
   a.sc = out->sc;
   a.fs = format_set(out);
+  a.norm = norm ? 1 : 0;
+  a.gamma = static_cast<const uint16_t*>(gamma);
+  a.eps = eps;
   hipError_t e = mm::launch_quantize(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "%s: launch failed: %s", who, hipGetErrorString(e));
   return MM_OK;
@@ -179,6 +186,15 @@ mm_status mm_quantize_act(const void* x_bf16, int64_t ldx, const int32_t* perm, 
 mm_status mm_quantize_weight(const void* w_bf16, int64_t ldw, const int32_t* perm, const mm_mx_tensor* out,
                              void* stream) {
   return quantize(w_bf16, ldw, perm, out, stream, "mm_quantize_weight");
+}
+
+mm_status mm_rmsnorm_quantize_act(const void* x_bf16, int64_t ldx, const void* gamma_bf16, float eps,
+                                  const int32_t* perm, const mm_mx_tensor* out, void* stream) {
+  if (!gamma_bf16) {
+    g_err[0] = 0;
+    return fail(MM_ERR_NULL, "mm_rmsnorm_quantize_act: gamma is NULL");
+  }
+  return quantize(x_bf16, ldx, perm, out, stream, "mm_rmsnorm_quantize_act", gamma_bf16, eps);
 }
 
 mm_status mm_gemm(const mm_mx_tensor* a, const mm_mx_tensor* w, void* y_bf16, int64_t ldy, void* stream) {
@@ -282,6 +298,7 @@ const char* mm_status_str(mm_status s) {
     case MM_ERR_FORMAT: return "MM_ERR_FORMAT";
     case MM_ERR_DEVICE: return "MM_ERR_DEVICE";
     case MM_ERR_WORKSPACE: return "MM_ERR_WORKSPACE";
+    case MM_ERR_VALUE: return "MM_ERR_VALUE";
   }
   return "MM_ERR_UNKNOWN";
 }

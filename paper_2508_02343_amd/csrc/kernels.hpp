@@ -40,6 +40,11 @@ struct QuantArgs {
   uint8_t* q[3];
   uint8_t* sc;
   int fs;  // format set: bit 0 the 6-bit group is E2M3 (else E3M2), bit 1 the 8-bit group is E5M2 (else E4M3)
+  // RMSNorm before the quantisation (norm != 0): x -> bf16(gamma * bf16(x * r)),
+  // r = fp32(1 / sqrt(mean(x^2) + eps)) per row, gamma bf16 [K] in channel order
+  int norm;
+  const uint16_t* gamma;
+  float eps;
 };
 
 // One quantised GEMM operand.

@@ -22,6 +22,17 @@
 //    clamped to 448 * scale, which is exact in bf16;
 //  - consecutive lanes own consecutive blocks, so a wavefront's code stores
 //    cover a contiguous span of each group.
+//
+// With the RMSNorm fused in front (the norm variant, App. D.2): the waves
+// sum each staged row's squares in fp64 (a row split across several waves),
+// every thread forms its row's factor r = fp32(1 / sqrt(mean(x^2) + eps)),
+// and every gathered element becomes bf16(gamma * bf16(x * r)) (fp32
+// products, round to nearest even) before the block absmax.  The weights in
+// block order (gamma gathered by sigma) sit in LDS, four 16-byte pieces per
+// block at (piece * nblk + block) * 16 so a wavefront's reads are
+// conflict-free, in the unused tail of stage 0 when it has room; otherwise
+// (one wide row per pass) each thread keeps its block's 32 weights in
+// registers.
 #include "kernels.hpp"
 
 namespace mm {
@@ -40,6 +51,12 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // many bytes (rpp * K * 2).
 constexpr int kStageOff = 32768;
 constexpr int kMaxChunks = 4;  // 16-byte loads per thread per pass
+constexpr int kMaxRowSlots = 256;  // row square sums of one pass (rows per pass, or waves, never exceed this)
+// dynamic LDS at most: two stages, the dummy slot and the row square sums; or
+// one 64 KB row, the dummy slot, 16 (row, part) sums and its 64 KB of weights
+constexpr int kMaxLds = 2 * (2 * kStageOff) + 16 + 8 * 16;
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // LDS pointers built from 32-bit byte addresses (the base already added)
 typedef const __attribute__((address_space(3))) uint16_t lds_u16_t;
@@ -82,9 +99,9 @@ __device__ __forceinline__ void zero_tail(const QuantArgs& a, int64_t step, int6
 // Quantise block b (local to its group) of row n from LDS stage kStage; rows
 // past a.rows are padding and quantise an all-zero block.  The thread that
 // owns a group's last block also zeroes the padding blocks of that step.
-template <int kStage>
+template <int kStage, bool kNorm>
 __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, bool last, const QuantArgs& a,
-                                               int64_t n, int b, int gstep0) {
+                                               int64_t n, int b, int gstep0, const uint32_t (&gpk)[16], float rn) {
   // gather: the block's 32 permuted channels, all reads issued before any
   // is used, then packed as 16 bf16 pairs
   uint16_t e[32];
@@ -98,8 +115,28 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
     u16x2 v;
     v.x = e[2 * i];
     v.y = e[2 * i + 1];
-    d[i] = pad_row ? 0u : __builtin_bit_cast(uint32_t, v);
+    d[i] = __builtin_bit_cast(uint32_t, v);
   }
+  if constexpr (kNorm) {
+    // bf16(gamma * bf16(x * r)): fp32 products, each rounded to nearest even;
+    // four pairs at a time, so the temporaries of all sixteen are never live
+    // together
+#pragma unroll
+    for (int i0 = 0; i0 < 16; i0 += 4) {
+#pragma unroll
+      for (int i = i0; i < i0 + 4; ++i) {
+        const uint32_t w = d[i];
+        const f32x2 t = {__uint_as_float(w << 16) * rn, __uint_as_float(w & 0xFFFF0000u) * rn};
+        const uint32_t y = __builtin_bit_cast(uint32_t, __builtin_convertvector(t, bf16x2));
+        const f32x2 u = {__uint_as_float(y << 16) * __uint_as_float(gpk[i] << 16),
+                         __uint_as_float(y & 0xFFFF0000u) * __uint_as_float(gpk[i] & 0xFFFF0000u)};
+        d[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(u, bf16x2));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) d[i] = pad_row ? 0u : d[i];
 
   // absmax: bf16 magnitudes compare as unsigned integers
   uint32_t m[16];
@@ -195,8 +232,57 @@ __device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int g
 // passes.  kPipe: two LDS stages of rpp * K * 2 <= kStageOff bytes, loads of
 // the next pass overlap the current one; otherwise gridDim.x equals the
 // number of passes and one stage holds up to 2 * kStageOff bytes.
-template <int kMaxThreads, bool kPipe>
-__global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a, int rpp) {
+// Sums of squares of the rpp rows staged at byte offset stage_off, spread
+// over the workgroup's W waves: with rpp <= W each row gets W / rpp waves,
+// each summing one contiguous part of it; otherwise each wave sums whole rows
+// (rows strided by W).  Every (row, part) sum goes to slot
+// row * row_parts(rpp, W) + part at sq_off; squares of bf16 values are exact
+// in fp64, and the sums use four accumulators per lane and a fixed shuffle
+// tree, so the result does not depend on timing.
+__device__ __forceinline__ int row_parts(int rpp, int W) { return rpp <= W ? W / rpp : 1; }
+
+__device__ __forceinline__ void row_square_sums(const u32x4* lds4, uint32_t stage_off, uint32_t sq_off, int rpp, int K) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, W = blockDim.x >> 6;
+  const int chunks = K >> 3;
+  const int parts = row_parts(rpp, W);
+  const int first = rpp <= W ? wave / parts : wave;
+  const int step = rpp <= W ? rpp : W;  // loop once when rows get several waves
+  for (int pr = first; pr < rpp; pr += step) {
+    const int part = rpp <= W ? wave % parts : 0;
+    const int c0 = part * chunks / parts, c1 = (part + 1) * chunks / parts;
+    const u32x4* row = lds4 + ((stage_off + (uint32_t)pr * K * 2) >> 4);
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int c = c0 + lane; c < c1; c += 64) {
+      const u32x4 v = row[c];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const double lo = (double)__uint_as_float(v[k] << 16), hi = (double)__uint_as_float(v[k] & 0xFFFF0000u);
+        acc[k] += lo * lo;
+        acc[k] += hi * hi;
+      }
+    }
+    double s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) reinterpret_cast<__attribute__((address_space(3))) double*>((uintptr_t)sq_off)[pr * parts + part] = s;
+    if (rpp <= W) break;
+  }
+}
+
+// fp32 row factor of pass-row pr from its part sums (after a barrier): the
+// same operations, in the same order, in every thread of the row.
+__device__ __forceinline__ float row_factor(uint32_t sq_off, int pr, int rpp, int K, float eps) {
+  const int parts = row_parts(rpp, blockDim.x >> 6);
+  const __attribute__((address_space(3))) double* sq =
+      reinterpret_cast<const __attribute__((address_space(3))) double*>((uintptr_t)sq_off) + pr * parts;
+  double s = sq[0];
+  for (int k = 1; k < parts; ++k) s += sq[k];
+  return (float)(1.0 / sqrt(s / (double)K + (double)eps));
+}
+
+// kNorm: 0 plain; 1 RMSNorm with the weights in registers; 2 RMSNorm with the
+// block-order weights in LDS at byte offset gamma_off.
+template <int kMaxThreads, bool kPipe, int kNorm>
+__global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a, int rpp, int gamma_off) {
   extern __shared__ u32x4 lds4[];
   const int tid = threadIdx.x;
   const int T = blockDim.x;
@@ -224,6 +310,30 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   // factored out and re-added before every LDS read
 #pragma unroll
   for (int i = 0; i < 32; ++i) asm volatile("" : "+v"(addr[i]));
+  // the norm weights of this thread's block, gathered by sigma, as bf16 pairs
+  // (kNorm 2: written once to LDS by the threads of pass-row 0)
+  uint32_t gpk[16];
+  if constexpr (kNorm != 0) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int4 v = *reinterpret_cast<const int4*>(a.perm + (active ? blk : 0) * 32 + 4 * q);
+      const int p[4] = {v.x, v.y, v.z, v.w};
+      uint32_t g[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) g[i] = a.gamma[(unsigned)p[i] < (unsigned)K ? p[i] : 0];
+      gpk[2 * q] = g[0] | (g[1] << 16);
+      gpk[2 * q + 1] = g[2] | (g[3] << 16);
+    }
+    if constexpr (kNorm == 2) {
+      if (active && prow == 0)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          lds4[(gamma_off >> 4) + q * nblk + blk] = u32x4{gpk[4 * q], gpk[4 * q + 1], gpk[4 * q + 2], gpk[4 * q + 3]};
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) gpk[i] = 0u;
+  }
   const int group = blk < a.nb[0] ? 0 : (blk < a.nb[0] + a.nb[1] ? 1 : 2);
   const int b = blk - (group >= 1 ? a.nb[0] : 0) - (group >= 2 ? a.nb[1] : 0);  // block within its group
   const int gstep0 = (group >= 1 ? a.steps[0] : 0) + (group >= 2 ? a.steps[1] : 0);
@@ -235,6 +345,8 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   // and LDS write is unconditional and in bounds
   const int chunks_per_row = K >> 3;
   const uint32_t dummy = (uint32_t)((kPipe ? kStageOff : 0) + stage_bytes);
+  // row square sums of the pass being quantised (norm variant), after the dummy slot
+  const uint32_t sq_off = (uint32_t)(uintptr_t)lds4 + dummy + 16;
   u32x4 buf[kMaxChunks];
 #define MM_LOAD_PASS(P)                                                                              \
   {                                                                                                  \
@@ -277,12 +389,32 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
   for (int i = 0; q < q_end; ++i, q += stride) {
     const bool more = kPipe && q + stride < q_end;
     if (more) MM_LOAD_PASS(q + stride);
+    float rn = 0.0f;
+    if constexpr (kNorm != 0) {
+      row_square_sums(lds4, (uint32_t)((i & 1) * kStageOff), sq_off, rpp, K);
+      __syncthreads();
+      rn = row_factor(sq_off, active ? prow : 0, rpp, K, a.eps);
+    }
     const int64_t row = q * rpp + prow;
     if (active && row < a.rp) {
+      uint32_t gq[16];
+      if constexpr (kNorm == 2) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const u32x4 v = lds4[(gamma_off >> 4) + k * nblk + blk];
+          gq[4 * k] = v[0];
+          gq[4 * k + 1] = v[1];
+          gq[4 * k + 2] = v[2];
+          gq[4 * k + 3] = v[3];
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) gq[k] = gpk[k];
+      }
       if ((i & 1) == 0)
-        quantize_block<0>(addr, group, last, a, row, b, gstep0);
+        quantize_block<0, kNorm != 0>(addr, group, last, a, row, b, gstep0, gq, rn);
       else
-        quantize_block<1>(addr, group, last, a, row, b, gstep0);
+        quantize_block<1, kNorm != 0>(addr, group, last, a, row, b, gstep0, gq, rn);
     }
     if (more) MM_STORE_PASS((i + 1) & 1);
     __syncthreads();
@@ -292,19 +424,20 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
 }
 
 // Allow more than 64 KB of dynamic LDS (two 32 KB stages plus the dummy
-// slot, or one 64 KB row).
-template <int kMaxThreads, bool kPipe>
+// slot and the row square sums, or one wide row and its weights).
+template <int kMaxThreads, bool kPipe, int kNorm>
 static hipError_t allow_lds(size_t bytes) {
   static bool done = false;
   if (done || bytes <= 65536) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(quantize_rows_kernel<kMaxThreads, kPipe>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kStageOff + 16);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(quantize_rows_kernel<kMaxThreads, kPipe, kNorm>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds);
   if (e == hipSuccess) done = true;
   return e;
 }
 
 // Workgroups of the pipelined kernel resident on the current device at once
 // (per-CU occupancy times CU count), cached per thread for the last shape.
+template <int kNorm>
 static hipError_t resident_workgroups(int T, size_t lds, int* cap) {
   thread_local int last_dev = -1, last_T = 0, last_cap = 0;
   thread_local size_t last_lds = 0;
@@ -313,7 +446,7 @@ static hipError_t resident_workgroups(int T, size_t lds, int* cap) {
   if (e != hipSuccess) return e;
   if (dev != last_dev || T != last_T || lds != last_lds) {
     int per_cu = 0, cus = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_rows_kernel<512, true>, T, lds);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_rows_kernel<512, true, kNorm>, T, lds);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
@@ -326,18 +459,43 @@ static hipError_t resident_workgroups(int T, size_t lds, int* cap) {
   return hipSuccess;
 }
 
-hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
-  if (a.rows == 0) return hipSuccess;
+template <int kNorm>
+static hipError_t launch_pipelined(const QuantArgs& a, int rpp, int T, size_t lds, int gamma_off, hipStream_t stream) {
+  hipError_t e = allow_lds<512, true, kNorm>(lds);
+  if (e != hipSuccess) return e;
+  // one wave of workgroups: as many as the chip holds at once
+  int cap = 0;
+  e = resident_workgroups<kNorm>(T, lds, &cap);
+  if (e != hipSuccess) return e;
+  const int64_t passes = (a.rp + rpp - 1) / rpp;
+  const int64_t grid = passes < cap ? passes : cap;
+  hipLaunchKernelGGL((quantize_rows_kernel<512, true, kNorm>), dim3((unsigned)grid), dim3(T), lds, stream, a, rpp,
+                     gamma_off);
+  return hipGetLastError();
+}
+
+static hipError_t launch_quantize_rows(const QuantArgs& a, hipStream_t stream) {
   const int K = a.K;
   const int nblk = K >> 5;
+  const bool norm = a.norm != 0;
   // A row wider than one stage (K > 16384) is quantised without overlap, one
-  // row per workgroup of K/32 threads (up to 1024).
+  // row per workgroup of K/32 threads (up to 1024); with the norm its weights
+  // follow the row, the dummy slot and the (row, part) sums in LDS.
   if (K * 2 > kStageOff) {
     const int T = (nblk + 63) / 64 * 64;
-    const size_t lds = (size_t)K * 2 + 16;
-    hipError_t e = allow_lds<1024, false>(lds);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((quantize_rows_kernel<1024, false>), dim3((unsigned)a.rp), dim3(T), lds, stream, a, 1);
+    const int gamma_off = K * 2 + 16 + 8 * 16;
+    if (norm) {
+      const size_t lds = (size_t)gamma_off + (size_t)K * 2;
+      hipError_t e = allow_lds<1024, false, 2>(lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((quantize_rows_kernel<1024, false, 2>), dim3((unsigned)a.rp), dim3(T), lds, stream, a, 1,
+                         gamma_off);
+    } else {
+      const size_t lds = (size_t)K * 2 + 16;
+      hipError_t e = allow_lds<1024, false, 0>(lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((quantize_rows_kernel<1024, false, 0>), dim3((unsigned)a.rp), dim3(T), lds, stream, a, 1, 0);
+    }
     return hipGetLastError();
   }
   // rows per pass: the fewest idle lanes (ties: more rows) among launches of
@@ -355,19 +513,21 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
     }
     if (t >= 256) break;
   }
+  if (rpp > kMaxRowSlots) return hipErrorInvalidValue;  // cannot happen: rpp * nblk <= 512
   const int T = (rpp * nblk + 63) / 64 * 64;
-  const int64_t passes = (a.rp + rpp - 1) / rpp;
-  // two stages plus the 16-byte dummy slot
-  const size_t lds = (size_t)kStageOff + (size_t)rpp * K * 2 + 16;
-  hipError_t e = allow_lds<512, true>(lds);
-  if (e != hipSuccess) return e;
-  // one wave of workgroups: as many as the chip holds at once
-  int cap = 0;
-  e = resident_workgroups(T, lds, &cap);
-  if (e != hipSuccess) return e;
-  const int64_t grid = passes < cap ? passes : cap;
-  hipLaunchKernelGGL((quantize_rows_kernel<512, true>), dim3((unsigned)grid), dim3(T), lds, stream, a, rpp);
-  return hipGetLastError();
+  // two stages plus the 16-byte dummy slot (and the (row, part) square sums)
+  size_t lds = (size_t)kStageOff + (size_t)rpp * K * 2 + 16;
+  if (!norm) return launch_pipelined<0>(a, rpp, T, lds, 0, stream);
+  const int slots = rpp > T / 64 ? rpp : T / 64;  // max(rpp, waves)
+  lds += (size_t)slots * 8;
+  // the block-order weights fit the unused tail of stage 0
+  if ((rpp + 1) * K * 2 <= kStageOff) return launch_pipelined<2>(a, rpp, T, lds, rpp * K * 2, stream);
+  return launch_pipelined<1>(a, rpp, T, lds, 0, stream);
+}
+
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream) {
+  if (a.rows == 0) return hipSuccess;
+  return launch_quantize_rows(a, stream);
 }
 
 }  // namespace mm

@@ -26,6 +26,7 @@ def _declared_functions():
 def test_header_declares_the_calls():
     names = _declared_functions()
     for n in ("mm_quantize_act", "mm_quantize_weight", "mm_gemm", "mm_calibrate", "mm_calibrate_workspace_size",
+              "mm_rmsnorm_quantize_act",
               "mm_status_str", "mm_last_error", "mm_abi_version"):
         assert n in names
 
@@ -34,7 +35,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(b.LIB_PATH)
     for n in _declared_functions():
         assert hasattr(lib, n), n
-    assert b.lib.mm_abi_version() == 4
+    assert b.lib.mm_abi_version() == 5
 
 
 def test_status_strings():
@@ -233,4 +234,25 @@ def test_calibrate_rejects_bad_arguments():
     assert _cal(ws=FAKE + 8) == "MM_ERR_ALIGN"
     assert _cal(perm=FAKE + 4) == "MM_ERR_ALIGN"
     assert _cal(split=FAKE + 2) == "MM_ERR_ALIGN"
+    assert b.lib.mm_last_error().decode()
+
+
+def _nq(d, x=FAKE, gamma=FAKE, eps=1e-5, perm=FAKE):
+    st = b.lib.mm_rmsnorm_quantize_act(ctypes.c_void_p(x), d.K, ctypes.c_void_p(gamma), ctypes.c_float(eps),
+                                       ctypes.c_void_p(perm), ctypes.byref(d), None)
+    return b.STATUS_NAMES[st]
+
+
+def test_rmsnorm_quantize_rejects_bad_arguments():
+    d = _tensor()
+    assert _nq(d, gamma=0) == "MM_ERR_NULL"
+    assert _nq(d, x=0) == "MM_ERR_NULL"
+    assert _nq(d, perm=0) == "MM_ERR_NULL"
+    for eps in (0.0, -1e-5, float("inf"), float("nan")):
+        assert _nq(d, eps=eps) == "MM_ERR_VALUE", eps
+    assert _nq(d, gamma=FAKE + 1) == "MM_ERR_ALIGN"
+    assert _nq(_tensor(split=(64, 16, 48))) == "MM_ERR_SPLIT"
+    bad = _tensor()
+    bad.formats = b.MMFormats(7, 0)
+    assert _nq(bad) == "MM_ERR_FORMAT"
     assert b.lib.mm_last_error().decode()
