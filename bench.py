@@ -245,6 +245,30 @@ def main() -> int:
     norm_ms = timed(lambda i: B.rmsnorm_quantize_act(X[i % nbuf], gamma, 1e-5, perm, w.split, out=XQ[i % nbuf],
                                                      stream=stream), args.steps)
 
+    qkv = None
+    if w.name == "llama8b_attn_2048x4096x4096":
+        # Q, K and V projections of Llama-3-8B (4096 + 1024 + 1024 outputs) on one
+        # quantised activation: the weights stacked along N in one GEMM, against
+        # three GEMMs (weights resident: the same for both)
+        rng = np.random.default_rng([w.seed, 5])
+        parts = (4096, 1024, 1024)
+        wl = [W.f32_to_bf16_bits((rng.standard_normal((n, w.K)) * 0.02).astype(np.float32)) for n in parts]
+        wst = B.quantize_weight(to_bf16(np.concatenate(wl)), perm, w.split, stream=stream)
+        wsep = [B.quantize_weight(to_bf16(x), perm, w.split, stream=stream) for x in wl]
+        yst = torch.empty((w.M, sum(parts)), dtype=torch.bfloat16, device=dev)
+        ysep = [torch.empty((w.M, n), dtype=torch.bfloat16, device=dev) for n in parts]
+        st_ms = timed(lambda i: B.gemm(XQ[i % nbuf], wst, y=yst, stream=stream), args.steps)
+
+        def three(i):
+            for k in range(3):
+                B.gemm(XQ[i % nbuf], wsep[k], y=ysep[k], stream=stream)
+
+        sep_ms = timed(three, args.steps)
+        qflops = 2.0 * w.M * w.K * sum(parts)
+        qkv = {"N": list(parts), "stacked_ms": round(st_ms, 5), "separate_ms": round(sep_ms, 5),
+               "stacked_TFLOPs": round(qflops / (st_ms * 1e-3) / 1e12, 1),
+               "separate_TFLOPs": round(qflops / (sep_ms * 1e-3) / 1e12, 1)}
+
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     flops = 2.0 * w.M * w.N * w.K
     value = flops / (ms_per_step * 1e-3) / 1e12
@@ -287,6 +311,7 @@ def main() -> int:
                               "unit": "GB/s", "frac": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
                               "vs_plain_quantizer": round(norm_ms / quant_ms, 3)},
         "gemm_ms": round(gemm_ms, 5),
+        "shared_activation_qkv": qkv,
         "quant_share_of_kernel_time": round(quant_ms / (quant_ms + gemm_ms), 4),
         "weight_quantize": {"ms": round(wq_ms, 5), "GB/s": round(wq_gbps, 1)},
     }

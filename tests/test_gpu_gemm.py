@@ -146,3 +146,30 @@ def test_mixed_formats_are_rejected():
     w = b.quantize_weight(to_dev_bf16(wb), p, (96, 160, 96))
     with pytest.raises(b.MMError, match="MM_ERR_FORMAT"):
         b.gemm(a, w)
+
+
+@pytest.mark.parametrize("M", [8, 300])
+def test_stacked_qkv_equals_separate_gemms(M):
+    """Q, K and V share the activation's sigma and split, so their weights can
+    be stacked along N (Llama-3-8B: 4096 + 1024 + 1024 rows), quantised once and
+    multiplied in one launch; each column slice of that product equals,
+    bit for bit, the separate GEMM of the same quantised activation (every
+    output element sums the same K blocks in the same order)."""
+    b = _b()
+    K, split, parts = 4096, (3072, 768, 256), (4096, 1024, 1024)
+    rng = np.random.default_rng(M)
+    xb = W.LLAMA_ATTN.x_bits(M)
+    perm = W.LLAMA_ATTN.perm()
+    ws = [W.f32_to_bf16_bits((rng.standard_normal((n, K)) * 0.02).astype(np.float32)) for n in parts]
+    note(f"stacked QKV M={M}")
+    p = to_dev_perm(perm)
+    a = b.quantize_act(to_dev_bf16(xb), p, split)
+    stacked = b.gemm(a, b.quantize_weight(to_dev_bf16(np.concatenate(ws)), p, split))
+    sep = [b.gemm(a, b.quantize_weight(to_dev_bf16(wk), p, split)) for wk in ws]
+    torch.cuda.synchronize()
+    col = 0
+    for n, y in zip(parts, sep):
+        assert torch.equal(stacked[:, col:col + n], y), (M, col)
+        col += n
+    ref = O.gemm_mixed(O.quantize_mixed(xb, perm, split), O.quantize_mixed(ws[1], perm, split))
+    assert_gemm_close(y_to_f64(sep[1]), ref, ctx="K slice")
