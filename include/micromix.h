@@ -176,7 +176,7 @@ mm_status mm_quantize_act(const void* x_bf16, int64_t ldx, const int32_t* perm, 
  * (r evaluated in fp64 and rounded once to fp32; both products in fp32,
  * each rounded to nearest even), and y is quantised exactly as
  * mm_quantize_act would quantise it.
- *   gamma_bf16  device, bf16 [K] in the original channel order (2-byte
+ *   gamma_bf16  device, bf16 [K] in the original channel order (16-byte
  *               aligned, finite).
  *   eps         finite and > 0 (MM_ERR_VALUE otherwise).
  * The other arguments, the layout and the errors are those of

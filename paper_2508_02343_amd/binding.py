@@ -181,8 +181,8 @@ def quantize_act(x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | Non
 
 def rmsnorm_quantize_act(x: torch.Tensor, gamma: torch.Tensor, eps: float, perm: torch.Tensor, split,
                          out: MXTensor | None = None, stream=None, formats=DEFAULT_FORMATS) -> MXTensor:
-    """mm_rmsnorm_quantize_act: RMSNorm (bf16 weight gamma [K], eps) fused
-    with the reorder-and-quantize of bf16 activations."""
+    """mm_rmsnorm_quantize_act: RMSNorm (bf16 weight gamma [K], 16-byte
+    aligned, eps) fused with the reorder-and-quantize of bf16 activations."""
     if gamma.dtype != torch.bfloat16 or gamma.dim() != 1 or not gamma.is_contiguous() or gamma.numel() != x.shape[-1]:
         raise ValueError("gamma must be a contiguous bfloat16 tensor [K]")
     g = ctypes.c_void_p(gamma.data_ptr())

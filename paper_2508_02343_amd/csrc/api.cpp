@@ -103,7 +103,7 @@ mm_status quantize(const void* x, int64_t ldx, const int32_t* perm, const mm_mx_
   if (!aligned16(perm)) return fail(MM_ERR_ALIGN, "%s: perm must be 16-byte aligned", who);
   if (norm && !(eps > 0.0f && eps <= 3.0e38f))
     return fail(MM_ERR_VALUE, "%s: eps=%g must be finite and positive", who, (double)eps);
-  if (norm && ((uintptr_t)gamma & 1u)) return fail(MM_ERR_ALIGN, "%s: gamma must be 2-byte aligned", who);
+  if (norm && !aligned16(gamma)) return fail(MM_ERR_ALIGN, "%s: gamma must be 16-byte aligned", who);
   const Layout l = layout(out->rows, out->split);
   mm::QuantArgs a;
   a.x = static_cast<const uint16_t*>(x);

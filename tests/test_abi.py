@@ -251,6 +251,7 @@ def test_rmsnorm_quantize_rejects_bad_arguments():
     for eps in (0.0, -1e-5, float("inf"), float("nan")):
         assert _nq(d, eps=eps) == "MM_ERR_VALUE", eps
     assert _nq(d, gamma=FAKE + 1) == "MM_ERR_ALIGN"
+    assert _nq(d, gamma=FAKE + 8) == "MM_ERR_ALIGN"
     assert _nq(_tensor(split=(64, 16, 48))) == "MM_ERR_SPLIT"
     bad = _tensor()
     bad.formats = b.MMFormats(7, 0)
