@@ -13,9 +13,10 @@
 // step contiguously and block-major, so a tile's share of one step is a few
 // contiguous runs; it goes straight from global memory into LDS with
 // global_load_lds_dwordx4 (1 KB per wavefront instruction, plus one for the
-// step's E8M0 scale words), through a ring of as many stages as 160 KB of
-// LDS holds for the group (a stage is a whole layout step, or half of one
-// where whole steps would leave fewer than three stages).  Completion is
+// step's E8M0 scale words), through a ring of as many stages as the tile's
+// LDS share (160 KB, or 80 KB for 256 x 128 tiles) holds for the group (a
+// stage is a whole layout step, or half of one where whole steps would leave
+// fewer than three stages).  Completion is
 // tracked with explicit vmcnt waits and bare s_barrier (a __syncthreads fence
 // would wait for every load in flight).  The block-major layout makes the
 // fragment reads conflict-free: 16 consecutive lanes read 16 consecutive rows
@@ -28,7 +29,12 @@ namespace mm {
 
 namespace tiled {
 
-constexpr int kLdsBytes = 160 * 1024;
+// LDS per workgroup: all 160 KB for 256 x 256 tiles (one workgroup per CU);
+// 80 KB for 256 x 128 tiles, so two workgroups share a CU and one's pipeline
+// fill and epilogue overlap the other's K loop (measured: 15 % faster on
+// 4096 x 14336 x 4096, bit-identical results).
+__host__ __device__ constexpr int lds_bytes(int, int BM) { return BM == 128 ? 80 * 1024 : 160 * 1024; }
+__host__ __device__ constexpr int tiles_per_cu(int, int BM) { return BM == 128 ? 2 : 1; }
 
 // Eight wavefronts per workgroup, two per SIMD (while one waits at a barrier
 // or for LDS, the other's MFMAs run), all of them issuing the tile's DMA, in
@@ -51,14 +57,15 @@ template <int G, int BN, int BM>
 struct Plan {
   static constexpr int RB = step_row_bytes(G);  // bytes per row and layout step
   static constexpr int kRows = BN + BM;
-  static constexpr int US = kLdsBytes / (kRows * (RB + kStepBlocks)) >= 3 ? 1 : 2;  // sub-steps per layout step
+  static constexpr int kLds = lds_bytes(BN, BM);
+  static constexpr int US = kLds / (kRows * (RB + kStepBlocks)) >= 3 ? 1 : 2;  // sub-steps per layout step
   static constexpr int kBlocks = kStepBlocks / US;
   static constexpr int kSlices = kBlocks / 2;
   static constexpr int kGrpBytes = kRowGroup * RB / US;  // one row group, one sub-step
   static constexpr int kWBytes = BN / kRowGroup * kGrpBytes;
   static constexpr int kCodeBytes = kRows / kRowGroup * kGrpBytes;
   static constexpr int kStageBytes = kCodeBytes + kRows * kStepBlocks;  // + the step's scale words
-  static constexpr int kStages = kLdsBytes / kStageBytes > 8 ? 8 : kLdsBytes / kStageBytes;
+  static constexpr int kStages = kLds / kStageBytes > 8 ? 8 : kLds / kStageBytes;
   static constexpr int kWInstr = kWBytes / 1024;            // DMA instructions carrying weight codes
   static constexpr int NW = Shape<BN, BM>::NW;
   // DMA instruction i (1 KB each) belongs to wavefront i % NW: the first kRem
@@ -357,7 +364,8 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
 using namespace tiled;
 
 template <int BN, int BM, int FS>
-__global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(GemmArgs a, int tiles_n, int tiles_m) {
+__global__ __launch_bounds__(64 * tile_waves(BN, BM), tiles_per_cu(BN, BM)) void gemm_tiled_kernel(GemmArgs a, int tiles_n,
+                                                                                                     int tiles_m) {
   using SH = Shape<BN, BM>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
   constexpr int kGroupN = 4;  // weight tiles that share an XCD's L2 at a time
@@ -402,7 +410,7 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), 1) void gemm_tiled_kernel(
   // row m = r.  Rows are padded by 16 bytes: the fragment writes of 32 lanes
   // (32 rows) then fall on distinct banks.
   constexpr int kRowStride = BN * 2 + 16;
-  static_assert(BM * kRowStride <= kLdsBytes, "epilogue tile fits LDS");
+  static_assert(BM * kRowStride <= lds_bytes(BN, BM), "epilogue tile fits LDS");
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5, r = lane & 31;
 #pragma unroll
@@ -439,12 +447,13 @@ static hipError_t launch_tile_fs(const GemmArgs& a, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel<BN, BM, FS>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes(BN, BM));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int tn = (int)((a.w.rows + BN - 1) / BN), tm = (int)((a.x.rows + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM, FS>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads), kLdsBytes, stream, a,
+  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM, FS>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads),
+                     lds_bytes(BN, BM), stream, a,
                      tn, tm);
   return hipGetLastError();
 }
