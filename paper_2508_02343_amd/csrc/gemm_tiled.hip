@@ -29,12 +29,13 @@ namespace mm {
 
 namespace tiled {
 
-// LDS per workgroup: all 160 KB for 256 x 256 tiles (one workgroup per CU);
-// 80 KB for 256 x 128 tiles, so two workgroups share a CU and one's pipeline
-// fill and epilogue overlap the other's K loop (measured: 15 % faster on
-// 4096 x 14336 x 4096, bit-identical results).
-__host__ __device__ constexpr int lds_bytes(int, int BM) { return BM == 128 ? 80 * 1024 : 160 * 1024; }
-__host__ __device__ constexpr int tiles_per_cu(int, int BM) { return BM == 128 ? 2 : 1; }
+// LDS per workgroup for TPC workgroups per CU: all 160 KB (TPC = 1), or 80 KB
+// (TPC = 2, 256 x 128 tiles only) so that two workgroups share a CU and one's
+// pipeline fill and epilogue overlap the other's K loop.  The launch takes
+// TPC = 2 when the 256 x 128 tiles outnumber the CUs (measured on 4096 x
+// 14336 x 4096: 15 % faster), else the deeper ring of TPC = 1 (8 % faster on
+// 2048 x 4096 x 4096, one tile per CU); results are bit-identical.
+__host__ __device__ constexpr int lds_bytes(int tpc) { return tpc == 2 ? 80 * 1024 : 160 * 1024; }
 
 // Eight wavefronts per workgroup, two per SIMD (while one waits at a barrier
 // or for LDS, the other's MFMAs run), all of them issuing the tile's DMA, in
@@ -53,11 +54,11 @@ struct Shape {
 // Pipeline plan of group G for a BN x BM tile: a "sub-step" is a whole layout
 // step (four blocks, two 64-channel slices), or half of one where a whole
 // step would leave fewer than three stages in LDS.
-template <int G, int BN, int BM>
+template <int G, int BN, int BM, int TPC>
 struct Plan {
   static constexpr int RB = step_row_bytes(G);  // bytes per row and layout step
   static constexpr int kRows = BN + BM;
-  static constexpr int kLds = lds_bytes(BN, BM);
+  static constexpr int kLds = lds_bytes(TPC);
   static constexpr int US = kLds / (kRows * (RB + kStepBlocks)) >= 3 ? 1 : 2;  // sub-steps per layout step
   static constexpr int kBlocks = kStepBlocks / US;
   static constexpr int kSlices = kBlocks / 2;
@@ -115,9 +116,9 @@ __device__ __forceinline__ void dma16_s(uint32_t voff, const void* sbase, uint32
 }
 
 // Per-tile constants of the DMA of one group.
-template <int G, int BN, int BM>
+template <int G, int BN, int BM, int TPC>
 struct Dma {
-  using P = Plan<G, BN, BM>;
+  using P = Plan<G, BN, BM, TPC>;
   const uint8_t* code[2];       // weight / activation codes at the tile's first row group
   const uint8_t* sc[2];         // scales at the tile's first row
   int64_t rp[2];                // padded rows of each operand
@@ -127,10 +128,10 @@ struct Dma {
   int t0;                       // global layout-step index of the group's first step
 };
 
-template <int G, int BN, int BM>
-__device__ __forceinline__ Dma<G, BN, BM> make_dma(const GemmArgs& a, int64_t n0, int64_t m0, int wave, int lane) {
-  using P = Plan<G, BN, BM>;
-  Dma<G, BN, BM> d;
+template <int G, int BN, int BM, int TPC>
+__device__ __forceinline__ Dma<G, BN, BM, TPC> make_dma(const GemmArgs& a, int64_t n0, int64_t m0, int wave, int lane) {
+  using P = Plan<G, BN, BM, TPC>;
+  Dma<G, BN, BM, TPC> d;
   d.rp[0] = a.w.rp;
   d.rp[1] = a.x.rp;
   d.code[0] = a.w.q[G] + n0 * P::RB;
@@ -169,9 +170,9 @@ __device__ __forceinline__ Dma<G, BN, BM> make_dma(const GemmArgs& a, int64_t n0
 }
 
 // Issue the DMA of sub-step p into the LDS stage at byte address st.
-template <int G, int BN, int BM>
-__device__ __forceinline__ void issue(const Dma<G, BN, BM>& d, uint32_t st, int wave, int lane, int p) {
-  using P = Plan<G, BN, BM>;
+template <int G, int BN, int BM, int TPC>
+__device__ __forceinline__ void issue(const Dma<G, BN, BM, TPC>& d, uint32_t st, int wave, int lane, int p) {
+  using P = Plan<G, BN, BM, TPC>;
   p = __builtin_amdgcn_readfirstlane(p);  // wave-uniform: the bases below must be scalar
   const int64_t s = p / P::US;
   const int u = p % P::US;
@@ -232,9 +233,9 @@ using Acc = v16f[Shape<BN, BM>::TN][Shape<BN, BM>::TM];
 // All activation fragments of the sub-step are read first; weight fragments
 // are double-buffered: the next one is read while the MFMAs of the current
 // one run.
-template <int G, int BN, int BM, int FS>
+template <int G, int BN, int BM, int FS, int TPC>
 __device__ __forceinline__ void compute_step(uint32_t st, int u, int wn0, int wm0, Acc<BN, BM>& acc) {
-  using P = Plan<G, BN, BM>;
+  using P = Plan<G, BN, BM, TPC>;
   constexpr int TN = Shape<BN, BM>::TN, TM = Shape<BN, BM>::TM, SL = P::kSlices;
   constexpr int kSliceOff = G == 0 ? 1024 : (G == 1 ? 1536 : 2048);  // slice 1 starts two blocks on
   const int lane = threadIdx.x & 63;
@@ -287,10 +288,10 @@ struct Ahead {
 // Issue sub-step 0 of group G into a stage of its ring that does not overlap
 // the live bytes [live, live + live_bytes) of the group still computing, and
 // record the ring rotation that puts it there.
-template <int G, int BN, int BM>
+template <int G, int BN, int BM, int TPC>
 __device__ __forceinline__ void issue_first(const GemmArgs& a, uint32_t lds0, int64_t n0, int64_t m0, int wave,
                                             uint32_t live, uint32_t live_bytes, Ahead& ah) {
-  using P = Plan<G, BN, BM>;
+  using P = Plan<G, BN, BM, TPC>;
   int rot = 0;
   for (int k = 0; k < P::kStages; ++k) {
     const uint32_t lo = k * P::kStageBytes, hi = lo + P::kStageBytes;
@@ -300,22 +301,22 @@ __device__ __forceinline__ void issue_first(const GemmArgs& a, uint32_t lds0, in
     }
   }
   rot = __builtin_amdgcn_readfirstlane(rot);  // uniform; keeps the DMA's M0 value scalar
-  const Dma<G, BN, BM> d = make_dma<G, BN, BM>(a, n0, m0, wave, threadIdx.x & 63);
-  issue<G, BN, BM>(d, lds0 + rot * P::kStageBytes, wave, threadIdx.x & 63, 0);
+  const Dma<G, BN, BM, TPC> d = make_dma<G, BN, BM, TPC>(a, n0, m0, wave, threadIdx.x & 63);
+  issue<G, BN, BM, TPC>(d, lds0 + rot * P::kStageBytes, wave, threadIdx.x & 63, 0);
   ah.group = G;
   ah.rot = rot;
 }
 
-template <int G, int BN, int BM, int FS>
+template <int G, int BN, int BM, int FS, int TPC>
 __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int64_t n0, int64_t m0, int wave,
                                           int wn0, int wm0, Acc<BN, BM>& acc, Ahead& ah) {
-  using P = Plan<G, BN, BM>;
+  using P = Plan<G, BN, BM, TPC>;
   constexpr int NS = P::kStages;
   const int S = a.steps[G];
   if (S == 0) return;
   const int PS = S * P::US;  // sub-steps
   const int lane = threadIdx.x & 63;
-  const Dma<G, BN, BM> d = make_dma<G, BN, BM>(a, n0, m0, wave, lane);
+  const Dma<G, BN, BM, TPC> d = make_dma<G, BN, BM, TPC>(a, n0, m0, wave, lane);
   // sub-step q lives in stage (q + rot) % NS; sub-step 0 may already be in
   // flight (issued during the previous group's last sub-step)
   const bool first_ahead = ah.group == G;
@@ -323,7 +324,7 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
   auto stage = [&](int q) { return lds0 + (uint32_t)__builtin_amdgcn_readfirstlane(((q + rot) % NS) * P::kStageBytes); };
 
   for (int q = first_ahead ? 1 : 0; q < NS - 1; ++q)
-    if (q < PS) issue<G, BN, BM>(d, stage(q), wave, lane, q);
+    if (q < PS) issue<G, BN, BM, TPC>(d, stage(q), wave, lane, q);
 
   for (int p = 0; p < PS; ++p) {
     // sub-steps p+1 .. p+NS-2 may still be in flight; sub-step p must have
@@ -340,18 +341,18 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
     // refill the stage that sub-step p-1 used; during the last sub-step,
     // start the next non-empty group instead
     if (p + NS - 1 < PS) {
-      issue<G, BN, BM>(d, stage(p + NS - 1), wave, lane, p + NS - 1);
+      issue<G, BN, BM, TPC>(d, stage(p + NS - 1), wave, lane, p + NS - 1);
     } else if (p == PS - 1) {
       const uint32_t live = ((p + rot) % NS) * P::kStageBytes;
       if constexpr (G < 2) {
         if (a.steps[G + 1] > 0)
-          issue_first<G + 1, BN, BM>(a, lds0, n0, m0, wave, live, P::kStageBytes, ah);
+          issue_first<G + 1, BN, BM, TPC>(a, lds0, n0, m0, wave, live, P::kStageBytes, ah);
         else if constexpr (G == 0) {
-          if (a.steps[2] > 0) issue_first<2, BN, BM>(a, lds0, n0, m0, wave, live, P::kStageBytes, ah);
+          if (a.steps[2] > 0) issue_first<2, BN, BM, TPC>(a, lds0, n0, m0, wave, live, P::kStageBytes, ah);
         }
       }
     }
-    compute_step<G, BN, BM, FS>(stage(p), p % P::US, wn0, wm0, acc);
+    compute_step<G, BN, BM, FS, TPC>(stage(p), p % P::US, wn0, wm0, acc);
   }
   // the next group lays its stages out differently: every wave must be done
   // reading this group's LDS first
@@ -363,8 +364,8 @@ __device__ __forceinline__ void run_group(const GemmArgs& a, uint32_t lds0, int6
 
 using namespace tiled;
 
-template <int BN, int BM, int FS>
-__global__ __launch_bounds__(64 * tile_waves(BN, BM), tiles_per_cu(BN, BM)) void gemm_tiled_kernel(GemmArgs a, int tiles_n,
+template <int BN, int BM, int FS, int TPC>
+__global__ __launch_bounds__(64 * tile_waves(BN, BM), TPC) void gemm_tiled_kernel(GemmArgs a, int tiles_n,
                                                                                                      int tiles_m) {
   using SH = Shape<BN, BM>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
@@ -399,9 +400,9 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), tiles_per_cu(BN, BM)) void
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
   Ahead ah{-1, 0};
-  run_group<0, BN, BM, FS>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
-  run_group<1, BN, BM, FS>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
-  run_group<2, BN, BM, FS>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<0, BN, BM, FS, TPC>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<1, BN, BM, FS, TPC>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
+  run_group<2, BN, BM, FS, TPC>(a, lds0, n0, m0, wave, wn0, wm0, acc, ah);
 
   // Epilogue: the bf16 tile is assembled in LDS (free again after the last
   // group's closing barrier) and written out as whole rows, 16 bytes per
@@ -410,7 +411,7 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), tiles_per_cu(BN, BM)) void
   // row m = r.  Rows are padded by 16 bytes: the fragment writes of 32 lanes
   // (32 rows) then fall on distinct banks.
   constexpr int kRowStride = BN * 2 + 16;
-  static_assert(BM * kRowStride <= lds_bytes(BN, BM), "epilogue tile fits LDS");
+  static_assert(BM * kRowStride <= lds_bytes(TPC), "epilogue tile fits LDS");
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5, r = lane & 31;
 #pragma unroll
@@ -442,40 +443,60 @@ __global__ __launch_bounds__(64 * tile_waves(BN, BM), tiles_per_cu(BN, BM)) void
   }
 }
 
-template <int BN, int BM, int FS>
+template <int BN, int BM, int FS, int TPC>
 static hipError_t launch_tile_fs(const GemmArgs& a, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel<BN, BM, FS>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes(BN, BM));
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_tiled_kernel<BN, BM, FS, TPC>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes(TPC));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int tn = (int)((a.w.rows + BN - 1) / BN), tm = (int)((a.x.rows + BM - 1) / BM);
-  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM, FS>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads),
-                     lds_bytes(BN, BM), stream, a,
+  hipLaunchKernelGGL((gemm_tiled_kernel<BN, BM, FS, TPC>), dim3((unsigned)(tn * tm)), dim3(Shape<BN, BM>::kThreads),
+                     lds_bytes(TPC), stream, a,
                      tn, tm);
   return hipGetLastError();
 }
 
 // The format set is an instruction immediate: one kernel per set.
-template <int BN, int BM>
+template <int BN, int BM, int TPC>
 static hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
   switch (a.fs) {
-    case 0: return launch_tile_fs<BN, BM, 0>(a, stream);
-    case 1: return launch_tile_fs<BN, BM, 1>(a, stream);
-    case 2: return launch_tile_fs<BN, BM, 2>(a, stream);
-    case 3: return launch_tile_fs<BN, BM, 3>(a, stream);
-    default: return hipErrorInvalidValue;
+    case 0: return launch_tile_fs<BN, BM, 0, TPC>(a, stream);
+    case 1: return launch_tile_fs<BN, BM, 1, TPC>(a, stream);
+    case 2: return launch_tile_fs<BN, BM, 2, TPC>(a, stream);
+    case 3: return launch_tile_fs<BN, BM, 3, TPC>(a, stream);
   }
+  return hipErrorInvalidValue;
+}
+
+// CUs of the current device (cached per thread for the last device).
+static hipError_t device_cus(int* cus) {
+  thread_local int last_dev = -1, last_cus = 0;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev != last_dev) {
+    e = hipDeviceGetAttribute(&last_cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    last_dev = dev;
+  }
+  *cus = last_cus;
+  return hipSuccess;
 }
 
 hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t stream) {
   // 256 x 256 tiles when they still give every CU several tiles, else
-  // 256 x 128 (twice the tiles)
+  // 256 x 128 (twice the tiles), two per CU when they outnumber the CUs
   const int64_t t256 = ((a.w.rows + 255) / 256) * ((a.x.rows + 255) / 256);
-  if (t256 >= 768) return launch_tile<256, 256>(a, stream);
-  return launch_tile<256, 128>(a, stream);
+  if (t256 >= 768) return launch_tile<256, 256, 1>(a, stream);
+  int cus = 0;
+  hipError_t e = device_cus(&cus);
+  if (e != hipSuccess) return e;
+  const int64_t t128 = ((a.w.rows + 255) / 256) * ((a.x.rows + 127) / 128);
+  if (t128 > cus) return launch_tile<256, 128, 2>(a, stream);
+  return launch_tile<256, 128, 1>(a, stream);
 }
 
 }  // namespace mm
