@@ -32,17 +32,24 @@ def _b():
     return binding
 
 
-def _factors(xb, eps):
-    """fp32 row factors, and for rows near an fp32 midpoint the other candidate."""
-    r = O.rmsnorm_row_factor(xb, eps)
+def factor_candidates(r, K):
+    """fp32 roundings of float64 row factors r, and for factors within
+    4 K 2^-53 (relative) of an fp32 rounding midpoint the neighbour on the
+    other side of that midpoint (else the same value)."""
+    r = np.asarray(r, dtype=np.float64)
     r32 = r.astype(np.float32)
     up = np.nextafter(r32, np.float32(np.inf))
     dn = np.nextafter(r32, np.float32(0))
     mid_up = (r32.astype(np.float64) + up.astype(np.float64)) / 2
     mid_dn = (r32.astype(np.float64) + dn.astype(np.float64)) / 2
-    tol = 4.0 * xb.shape[1] * 2.0 ** -53 * r
+    tol = 4.0 * K * 2.0 ** -53 * r
     alt = np.where(np.abs(r - mid_up) <= tol, up, np.where(np.abs(r - mid_dn) <= tol, dn, r32))
     return r32, alt, alt != r32
+
+
+def _factors(xb, eps):
+    """fp32 row factors, and for rows near an fp32 midpoint the other candidate."""
+    return factor_candidates(O.rmsnorm_row_factor(xb, eps), xb.shape[1])
 
 
 def _run(xb, gb, eps, perm, split, formats=("E3M2", "E4M3"), ld_extra=0):
