@@ -425,11 +425,6 @@ def gemm_mixed(a: MXTensor, w: MXTensor) -> np.ndarray:
     return dequantize_mixed(a) @ dequantize_mixed(w).T
 
 
-def gemm_mixed_bf16(a: MXTensor, w: MXTensor) -> np.ndarray:
-    """The reference rounded once to bf16 (bit patterns), for reporting."""
-    return f64_to_bf16_bits(gemm_mixed(a, w))
-
-
 def gemm_tolerance(y_ref: np.ndarray) -> np.ndarray:
     """Elementwise bound |y - y_ref| <= 2^-8 |y_ref| + 1e-3 rms(y_ref)."""
     y_ref = np.asarray(y_ref, dtype=np.float64)

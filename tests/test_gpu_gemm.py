@@ -68,6 +68,35 @@ def test_ragged(M, N, split):
     _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
 
 
+@pytest.mark.parametrize("split", [(96, 160, 96), (352, 0, 0), (0, 352, 0), (0, 0, 352), (128, 0, 224)])
+@pytest.mark.parametrize("M,N", [(3000, 5400), (1000, 1000)])
+def test_ragged_large(M, N, split):
+    """Every output of shapes whose tile grids run the 256 x 256 tiles
+    (12 x 22 tiles, at least one per CU) and the 256 x 128 tiles (4 x 8),
+    both with ragged last tiles in M and N."""
+    note(f"ragged large M={M} N={N} split={split}")
+    xb, wb, perm = _rand_case(M, N, split, seed=M + N + split[1])
+    _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
+
+
+@pytest.mark.parametrize("M,N", [(3000, 5400), (1000, 1000)])
+def test_ragged_large_alternative_formats(M, N):
+    split, formats = (96, 160, 96), ("E2M3", "E5M2")
+    note(f"ragged large formats {formats} M={M} N={N}")
+    xb, wb, perm = _rand_case(M, N, split, seed=M + 2 * N)
+    b = _b()
+    p = to_dev_perm(perm)
+    a = b.quantize_act(to_dev_bf16(xb), p, split, formats=formats)
+    w = b.quantize_weight(to_dev_bf16(wb), p, split, formats=formats)
+    y = b.gemm(a, w)
+    torch.cuda.synchronize()
+    fm = (O.E2M1, O.FORMATS[formats[0]], O.FORMATS[formats[1]])
+    ra, rw = O.quantize_mixed(xb, perm, split, fm), O.quantize_mixed(wb, perm, split, fm)
+    assert_codes_equal(a, ra, ctx="A")
+    assert_codes_equal(w, rw, ctx="W")
+    assert_gemm_close(y_to_f64(y), O.gemm_mixed(ra, rw), ctx=f"{formats} M{M} N{N}")
+
+
 @pytest.mark.parametrize("w", W.decode_workloads(), ids=lambda w: w.name)
 def test_decode_configs(w):
     """Full activation and full weight on the GPU; oracle on 256 sampled
@@ -79,14 +108,17 @@ def test_decode_configs(w):
     torch.cuda.synchronize()
     cols = np.unique(np.concatenate([[0, w.N - 1], np.random.default_rng(2).choice(w.N, 254, replace=False)]))
     ra, rw = O.quantize_mixed(xb, perm, w.split), O.quantize_mixed(wb[cols], perm, w.split)
+    assert_codes_equal(a, ra, ctx=w.name + " A")
     assert_codes_equal(wq, rw, rows=cols, ctx=w.name + " W")
     assert_gemm_close(y_to_f64(y)[:, cols], O.gemm_mixed(ra, rw), ctx=w.name)
 
 
 @pytest.mark.parametrize("w", W.PREFILL, ids=lambda w: w.name)
 def test_prefill_configs_sampled(w):
-    """Full-size GEMM on the GPU; the oracle recomputes 64 x 64 sampled
-    outputs from the sampled activation and weight rows."""
+    """Full-size quantisers and GEMM on the GPU; the oracle quantises 64
+    sampled activation rows and 64 sampled weight rows (their codes and
+    scales must match the GPU's bytes) and recomputes the 64 x 64 outputs
+    they meet in."""
     note(w.name)
     xb, wb, perm = w.x_bits(), w.w_bits(), w.perm()
     a, wq = _gpu_pair(xb, wb, perm, w.split)
@@ -96,6 +128,8 @@ def test_prefill_configs_sampled(w):
     rows = np.unique(np.concatenate([[0, w.M - 1], rng.choice(w.M, 62, replace=False)]))
     cols = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, 62, replace=False)]))
     ra, rw = O.quantize_mixed(xb[rows], perm, w.split), O.quantize_mixed(wb[cols], perm, w.split)
+    assert_codes_equal(a, ra, rows=rows, ctx=w.name + " A")
+    assert_codes_equal(wq, rw, rows=cols, ctx=w.name + " W")
     assert_gemm_close(y_to_f64(y[torch.from_numpy(rows).cuda()])[:, cols], O.gemm_mixed(ra, rw), ctx=w.name)
 
 
