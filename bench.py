@@ -76,10 +76,10 @@ def gemm_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per GEMM launch from the committed rocprofv3 counter summary,
-    or None when the summary is missing or was taken on other kernel sources."""
-    path = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+def _profile_entry(fname: str, workload: str):
+    """A workload's entry of a committed rocprofv3 counter summary, or None
+    when the summary is missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", fname)
     try:
         with open(path) as fh:
             rec = json.load(fh)
@@ -88,35 +88,82 @@ def measured_traffic(workload: str):
     entry = rec.get(workload)
     if not entry or entry.get("source_hash") != gemm_source_hash():
         return None
-    return entry.get("hbm_bytes_per_launch")
+    return entry
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per GEMM launch (rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE,
+    scaled by a plain copy's counts), or None."""
+    e = _profile_entry("gemm_traffic.json", workload)
+    return None if e is None else e.get("hbm_bytes_per_launch")
+
+
+def measured_mfma_util(workload: str):
+    """Fraction of the GEMM's active cycles its matrix cores were busy
+    (rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE per SIMD),
+    with the clock the counters imply, or None."""
+    e = _profile_entry("gemm_mfma.json", workload)
+    return None if e is None else {"mfma_busy": e.get("mfma_busy"), "clock_GHz": e.get("clock_GHz")}
+
+
+def cpu_threads() -> tuple[int, int]:
+    """(threads used, os.cpu_count()): the host's cores, at most the 16 a
+    one-GPU share of a GPU host gets."""
+    n = os.cpu_count() or 1
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        avail = n
+    return max(1, min(avail, 16)), n
 
 
 def cpu_baseline(w, seconds: float) -> dict:
-    """The oracle (float64 numpy) on a bounded sample: quantise a slice of the
-    activation rows and multiply it with the (pre-quantised) weight."""
+    """The oracle (float64 numpy) on a bounded sample of the workload, its
+    BLAS pool set to the host's threads: the quantiser on a slice of the
+    activation rows (GB/s over the same algorithmic bytes the GPU kernel is
+    charged) and the GEMM of that slice with the full, pre-quantised weight
+    (GFLOPS); value is the whole step (quantise + GEMM) in the metric's unit."""
     from oracle import mx_oracle as O
 
+    threads, ncpu = cpu_threads()
     try:
-        from threadpoolctl import threadpool_info
-
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
     rows = min(w.M, 256)
     xb, wb, perm = w.x_bits(rows), w.w_bits(), w.perm()
-    wq = O.quantize_mixed(wb, perm, w.split)
-    n_iter, t0 = 0, time.perf_counter()
-    while True:
-        a = O.quantize_mixed(xb, perm, w.split)
-        O.gemm_mixed(a, wq)
-        n_iter += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    tflops = 2.0 * rows * w.N * w.K * n_iter / el / 1e12
-    return {"value": tflops, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{rows} of {w.M} activation rows x full weight [{w.N},{w.K}], quantise + GEMM, "
-                      f"{n_iter} iterations in {el:.1f} s"}
+
+    def run():
+        wq = O.quantize_mixed(wb, perm, w.split)
+
+        def loop(fn, budget):
+            fn()  # one untimed call first (allocator and BLAS warm-up)
+            n, t0 = 0, time.perf_counter()
+            while True:
+                out = fn()
+                n += 1
+                el = time.perf_counter() - t0
+                if el >= budget:
+                    return out, n, el
+
+        a, nq, tq = loop(lambda: O.quantize_mixed(xb, perm, w.split), seconds / 3)
+        _, ng, tg = loop(lambda: O.gemm_mixed(a, wq), 2 * seconds / 3)
+        return nq, tq, ng, tg
+
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=threads):
+            nq, tq, ng, tg = run()
+    else:  # pragma: no cover
+        nq, tq, ng, tg = run()
+    q_s, g_s = tq / nq, tg / ng
+    flops = 2.0 * rows * w.N * w.K
+    return {"value": flops / (q_s + g_s) / 1e12, "unit": "TFLOP/s", "cores": threads, "os_cpu_count": ncpu,
+            "kind": "oracle",
+            "quantize_GBps": round(quant_bytes(rows, w.K, w.split) / q_s / 1e9, 4),
+            "gemm_GFLOPS": round(flops / g_s / 1e9, 3),
+            "sample": f"{rows} of {w.M} activation rows x full weight [{w.N},{w.K}]: quantise {nq} times in "
+                      f"{tq:.1f} s, GEMM {ng} times in {tg:.1f} s (weight quantised once, untimed); "
+                      f"BLAS threads {threads}"}
 
 
 def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps: int = 10) -> dict:
@@ -150,6 +197,110 @@ def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps
             "bytes_per_call": nbytes, "split": split.cpu().tolist()}
 
 
+class Operands:
+    """One workload's device buffers: bf16 activations, their packed
+    quantised form, the packed (offline-quantised) weight and the bf16
+    output, in several sets rotated so the working set exceeds the cache."""
+
+    def __init__(self, B, w, dev, stream, min_set_mb: float):
+        import torch
+
+        self.B, self.w, self.stream = B, w, stream
+        xb, wb, perm_np = w.x_bits(), w.w_bits(), w.perm()
+        self.perm = torch.from_numpy(perm_np).to(dev)
+        x0, w0 = to_dev_bf16(xb, dev), to_dev_bf16(wb, dev)
+        del xb, wb
+        p4, p6, p8 = w.split
+        row = p4 // 2 + 3 * p6 // 4 + p8 + w.K // 32
+        set_bytes = w.M * w.K * 2 + w.M * row + w.N * row + w.M * w.N * 2
+        self.nbuf = n = max(1, int(np.ceil(min_set_mb * 1e6 / set_bytes)))
+        self.X = [x0] + [x0.clone() for _ in range(n - 1)]
+        self.XQ = [B.MXTensor.empty(w.M, w.K, w.split, device=dev) for _ in range(n)]
+        self.WQ = [B.MXTensor.empty(w.N, w.K, w.split, device=dev) for _ in range(n)]
+        self.Y = [torch.empty((w.M, w.N), dtype=torch.bfloat16, device=dev) for _ in range(n)]
+        # offline weight quantisation (once per weight), timed on its own
+        self.wq_ms = launch_stats(stream, lambda i: B.quantize_weight(w0, self.perm, w.split, out=self.WQ[i],
+                                                                      stream=stream), n, mean_only=True)
+        for k in range(n):
+            B.quantize_act(self.X[k], self.perm, w.split, out=self.XQ[k], stream=stream)
+        torch.cuda.synchronize()
+
+    def quant(self, i):
+        k = i % self.nbuf
+        self.B.quantize_act(self.X[k], self.perm, self.w.split, out=self.XQ[k], stream=self.stream)
+
+    def gemm(self, i):
+        k = i % self.nbuf
+        self.B.gemm(self.XQ[k], self.WQ[k], y=self.Y[k], stream=self.stream)
+
+    def step(self, i):
+        self.quant(i)
+        self.gemm(i)
+
+
+def to_dev_bf16(bits, dev):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
+def launch_stats(stream, fn, n: int, mean_only: bool = False):
+    """Launch durations of fn(0..n-1) on `stream`, from HIP events recorded
+    on that stream.  The mean comes from n back-to-back launches with one
+    event pair around all of them (what a kernel trace averages); the median
+    from a second pass with an event after every launch.  Returns (mean ms,
+    median ms), or the mean alone."""
+    import torch
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(n):
+        fn(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mean = e0.elapsed_time(e1) / n
+    if mean_only:
+        return mean
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record(stream)
+    for i in range(n):
+        fn(i)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    med = float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]))
+    return mean, med
+
+
+def gemm_roofline(w, mean_ms: float, median_ms: float) -> dict:
+    """The GEMM against its roofline: the bit mix's MFMA peak for prefill
+    shapes, HBM for the decode kernel (M <= 64)."""
+    flops = 2.0 * w.M * w.N * w.K
+    if w.M > DIRECT_MAX_M:
+        ach = flops / (mean_ms * 1e-3) / 1e12
+        peak = mix_peak_tflops(w.split)
+        r = {"bound": "mfma", "kernel": "mixed MX GEMM", "achieved": round(ach, 2), "peak": round(peak, 1),
+             "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+             "median_frac": round(flops / (median_ms * 1e-3) / 1e12 / peak, 4),
+             "mfma_util": measured_mfma_util(w.name)}
+    else:
+        nbytes = gemm_bytes(w.M, w.N, w.K, w.split)
+        ach = nbytes / (mean_ms * 1e-3) / 1e9
+        r = {"bound": "hbm", "kernel": "mixed MX GEMM (decode)", "achieved": round(ach, 1), "peak": PEAK_HBM,
+             "unit": "GB/s", "frac": round(ach / PEAK_HBM, 4),
+             "median_frac": round(nbytes / (median_ms * 1e-3) / 1e9 / PEAK_HBM, 4)}
+    r.update({"traffic": measured_traffic(w.name), "ms": round(mean_ms, 5), "median_ms": round(median_ms, 5),
+              "source_hash": gemm_source_hash()})
+    return r
+
+
+def quant_roofline(w, mean_ms: float, median_ms: float) -> dict:
+    qbytes = quant_bytes(w.M, w.K, w.split)
+    gbps = qbytes / (mean_ms * 1e-3) / 1e9
+    return {"kernel": "reorder-and-quantize (activation)", "ms": round(mean_ms, 5), "median_ms": round(median_ms, 5),
+            "achieved": round(gbps, 1), "peak": PEAK_HBM, "unit": "GB/s", "frac": round(gbps / PEAK_HBM, 4),
+            "bytes_per_launch": qbytes}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -158,6 +309,10 @@ def main() -> int:
     ap.add_argument("--workload", default="llama8b_attn_2048x4096x4096")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-qkv", action="store_true",
+                    help="skip the stacked-vs-separate Q/K/V GEMM comparison (attention shape)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the per-configuration table of the other prefill shapes")
     ap.add_argument("--min-working-set-mb", type=float, default=768.0)
     ap.add_argument("--calibration-rows", type=int, default=32768,
                     help="calibration tokens for the offline mm_calibrate timing (0 skips it)")
@@ -168,6 +323,7 @@ def main() -> int:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}, WORLD_SIZE {world})", file=sys.stderr)
         return 2
+    n_time = max(args.steps, 50)  # per-kernel statistics over at least 50 launches
 
     import torch
 
@@ -177,21 +333,6 @@ def main() -> int:
     w = W.BY_NAME[args.workload]
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
-    xb, wb, perm_np = w.x_bits(), w.w_bits(), w.perm()
-    to_bf16 = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
-    x0, w0 = to_bf16(xb), to_bf16(wb)
-    perm = torch.from_numpy(perm_np).to(dev)
-
-    p4, p6, p8 = w.split
-    set_bytes = (w.M * w.K * 2 + w.M * (p4 // 2 + 3 * p6 // 4 + p8 + w.K // 32)
-                 + w.N * (p4 // 2 + 3 * p6 // 4 + p8 + w.K // 32) + w.M * w.N * 2)
-    nbuf = max(1, int(np.ceil(args.min_working_set_mb * 1e6 / set_bytes)))
-    X = [x0.clone() for _ in range(nbuf)]
-    XQ = [B.MXTensor.empty(w.M, w.K, w.split, device=dev) for _ in range(nbuf)]
-    WQ = [B.MXTensor.empty(w.N, w.K, w.split, device=dev) for _ in range(nbuf)]
-    Y = [torch.empty((w.M, w.N), dtype=torch.bfloat16, device=dev) for _ in range(nbuf)]
-    del x0
-
     stream = torch.cuda.current_stream()
     # a plain device copy of known size: under rocprofv3 --pmc its FETCH_SIZE /
     # WRITE_SIZE give the scale factor for the GEMM's counters
@@ -199,94 +340,87 @@ def main() -> int:
     calib_dst = torch.empty_like(calib)
     calib_dst.copy_(calib)
     del calib, calib_dst
-    # offline weight quantisation (once per weight), timed on its own
-    ew0, ew1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ew0.record(stream)
-    for k in range(nbuf):
-        B.quantize_weight(w0, perm, w.split, out=WQ[k], stream=stream)
-    ew1.record(stream)
-    torch.cuda.synchronize()
-    wq_ms = ew0.elapsed_time(ew1) / nbuf
-    del w0
 
-    def step(i):
-        k = i % nbuf
-        B.quantize_act(X[k], perm, w.split, out=XQ[k], stream=stream)
-        B.gemm(XQ[k], WQ[k], y=Y[k], stream=stream)
-
-    def timed(fn, n):
-        """Average duration of n back-to-back launches, HIP events on the
-        stream the kernels run on."""
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for i in range(n):
-            fn(i)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n
-
+    ops = Operands(B, w, dev, stream, args.min_working_set_mb)
     for i in range(args.warmup):
-        step(i)
+        ops.step(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i)
+        ops.step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
-    # per-kernel average launch durations: each kernel alone, back to back over
-    # the same rotated buffers (no event between launches)
-    quant_ms = timed(lambda i: B.quantize_act(X[i % nbuf], perm, w.split, out=XQ[i % nbuf], stream=stream),
-                     args.steps)
-    gemm_ms = timed(lambda i: B.gemm(XQ[i % nbuf], WQ[i % nbuf], y=Y[i % nbuf], stream=stream), args.steps)
+    # each kernel alone, back to back over the same rotated buffers
+    quant_ms, quant_med = launch_stats(stream, ops.quant, n_time)
+    gemm_ms, gemm_med = launch_stats(stream, ops.gemm, n_time)
     # the same quantiser with the layer's RMSNorm fused in front (weight ~ 1 + N(0, 0.25^2), eps 1e-5)
     g_np = (1.0 + 0.25 * np.random.default_rng([w.seed, 9]).standard_normal(w.K)).astype(np.float32)
-    gamma = to_bf16(W.f32_to_bf16_bits(g_np))
-    norm_ms = timed(lambda i: B.rmsnorm_quantize_act(X[i % nbuf], gamma, 1e-5, perm, w.split, out=XQ[i % nbuf],
-                                                     stream=stream), args.steps)
+    gamma = to_dev_bf16(W.f32_to_bf16_bits(g_np), dev)
+    norm_ms, norm_med = launch_stats(
+        stream, lambda i: B.rmsnorm_quantize_act(ops.X[i % ops.nbuf], gamma, 1e-5, ops.perm, w.split,
+                                                 out=ops.XQ[i % ops.nbuf], stream=stream), n_time)
 
     qkv = None
-    if w.name == "llama8b_attn_2048x4096x4096":
+    if w.name == "llama8b_attn_2048x4096x4096" and not args.no_qkv:
         # Q, K and V projections of Llama-3-8B (4096 + 1024 + 1024 outputs) on one
         # quantised activation: the weights stacked along N in one GEMM, against
         # three GEMMs (weights resident: the same for both)
         rng = np.random.default_rng([w.seed, 5])
         parts = (4096, 1024, 1024)
         wl = [W.f32_to_bf16_bits((rng.standard_normal((n, w.K)) * 0.02).astype(np.float32)) for n in parts]
-        wst = B.quantize_weight(to_bf16(np.concatenate(wl)), perm, w.split, stream=stream)
-        wsep = [B.quantize_weight(to_bf16(x), perm, w.split, stream=stream) for x in wl]
+        wst = B.quantize_weight(to_dev_bf16(np.concatenate(wl), dev), ops.perm, w.split, stream=stream)
+        wsep = [B.quantize_weight(to_dev_bf16(x, dev), ops.perm, w.split, stream=stream) for x in wl]
         yst = torch.empty((w.M, sum(parts)), dtype=torch.bfloat16, device=dev)
         ysep = [torch.empty((w.M, n), dtype=torch.bfloat16, device=dev) for n in parts]
-        st_ms = timed(lambda i: B.gemm(XQ[i % nbuf], wst, y=yst, stream=stream), args.steps)
+        st_ms = launch_stats(stream, lambda i: B.gemm(ops.XQ[i % ops.nbuf], wst, y=yst, stream=stream), n_time,
+                             mean_only=True)
 
         def three(i):
             for k in range(3):
-                B.gemm(XQ[i % nbuf], wsep[k], y=ysep[k], stream=stream)
+                B.gemm(ops.XQ[i % ops.nbuf], wsep[k], y=ysep[k], stream=stream)
 
-        sep_ms = timed(three, args.steps)
+        sep_ms = launch_stats(stream, three, n_time, mean_only=True)
         qflops = 2.0 * w.M * w.K * sum(parts)
         qkv = {"N": list(parts), "stacked_ms": round(st_ms, 5), "separate_ms": round(sep_ms, 5),
                "stacked_TFLOPs": round(qflops / (st_ms * 1e-3) / 1e12, 1),
                "separate_TFLOPs": round(qflops / (sep_ms * 1e-3) / 1e12, 1)}
+        del wst, wsep, yst, ysep
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     flops = 2.0 * w.M * w.N * w.K
     value = flops / (ms_per_step * 1e-3) / 1e12
-    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
-    peak = mix_peak_tflops(w.split)
-    qbytes = quant_bytes(w.M, w.K, w.split)
-    quant_gbps = qbytes / (quant_ms * 1e-3) / 1e9
-    wq_gbps = quant_bytes(w.N, w.K, w.split) / (wq_ms * 1e-3) / 1e9
+    quant = quant_roofline(w, quant_ms, quant_med)
+    qbytes = quant["bytes_per_launch"]
+    wq_gbps = quant_bytes(w.N, w.K, w.split) / (ops.wq_ms * 1e-3) / 1e9
 
-    if w.M > DIRECT_MAX_M:  # prefill: the block-scaled MFMA peak for the bit mix
-        roofline = {"bound": "mfma", "kernel": "mixed MX GEMM", "achieved": round(gemm_tflops, 2),
-                    "peak": round(peak, 1), "unit": "TFLOP/s", "frac": round(gemm_tflops / peak, 4),
-                    "traffic": measured_traffic(w.name), "source_hash": gemm_source_hash()}
-    else:  # decode: HBM bandwidth over the packed weight (and the small A / Y terms)
-        gbps = gemm_bytes(w.M, w.N, w.K, w.split) / (gemm_ms * 1e-3) / 1e9
-        roofline = {"bound": "hbm", "kernel": "mixed MX GEMM (decode)", "achieved": round(gbps, 1),
-                    "peak": PEAK_HBM, "unit": "GB/s", "frac": round(gbps / PEAK_HBM, 4),
-                    "traffic": measured_traffic(w.name), "source_hash": gemm_source_hash()}
+    def config_row(wl, q_mean, q_med, g_mean, g_med):
+        g = gemm_roofline(wl, g_mean, g_med)
+        q = quant_roofline(wl, q_mean, q_med)
+        return {"workload": wl.name, "M": wl.M, "K": wl.K, "N": wl.N, "split": list(wl.split),
+                "gemm": {k: g[k] for k in ("ms", "median_ms", "achieved", "peak", "unit", "frac", "median_frac",
+                                           "mfma_util", "traffic") if k in g},
+                "quantizer": {k: q[k] for k in ("ms", "median_ms", "achieved", "unit", "frac")},
+                "quant_to_gemm_time": round(q_med / g_med, 4),
+                "quant_share_of_kernel_time": round(q_med / (q_med + g_med), 4)}
+
+    sweep = None
+    if not args.no_sweep and w.M > DIRECT_MAX_M:
+        # the other prefill shapes, each kernel timed the same way
+        sweep = []
+        for wl in W.PREFILL:
+            if wl.name == w.name:
+                sweep.append(config_row(wl, quant_ms, quant_med, gemm_ms, gemm_med))
+                continue
+            o2 = Operands(B, wl, dev, stream, args.min_working_set_mb)
+            for i in range(args.warmup):
+                o2.step(i)
+            q2 = launch_stats(stream, o2.quant, n_time)
+            g2 = launch_stats(stream, o2.gemm, n_time)
+            sweep.append(config_row(wl, *q2, *g2))
+            del o2
+            torch.cuda.empty_cache()
+
     out = {
         "metric": "mixed MX GEMM TFLOPS (+quantizer GB/s) on Llama-8B/Qwen-32B layer shapes",
         "value": round(value, 2),
@@ -301,19 +435,21 @@ def main() -> int:
         "dtype": "mxfp4/mxfp6/mxfp8 (e2m1/e3m2/e4m3), fp32 accumulate, bf16 in/out",
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "split": list(w.split),
-                   "x_dist": w.x_dist, "rotated_buffer_sets": nbuf},
-        "roofline": roofline,
-        "quantizer": {"kernel": "reorder-and-quantize (activation)", "ms": round(quant_ms, 5),
-                      "achieved": round(quant_gbps, 1), "peak": PEAK_HBM, "unit": "GB/s",
-                      "frac": round(quant_gbps / PEAK_HBM, 4), "bytes_per_launch": qbytes},
+                   "x_dist": w.x_dist, "rotated_buffer_sets": ops.nbuf},
+        "roofline": gemm_roofline(w, gemm_ms, gemm_med),
+        "quantizer": quant,
         "rmsnorm_quantizer": {"kernel": "RMSNorm fused with reorder-and-quantize", "ms": round(norm_ms, 5),
+                              "median_ms": round(norm_med, 5),
                               "achieved": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM,
                               "unit": "GB/s", "frac": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
                               "vs_plain_quantizer": round(norm_ms / quant_ms, 3)},
         "gemm_ms": round(gemm_ms, 5),
+        "quant_share_of_kernel_time": round(quant_med / (quant_med + gemm_med), 4),
+        "prefill_configs": sweep,
         "shared_activation_qkv": qkv,
-        "quant_share_of_kernel_time": round(quant_ms / (quant_ms + gemm_ms), 4),
-        "weight_quantize": {"ms": round(wq_ms, 5), "GB/s": round(wq_gbps, 1)},
+        "weight_quantize": {"ms": round(ops.wq_ms, 5), "GB/s": round(wq_gbps, 1)},
+        "timing": f"per-kernel ms: mean of {n_time} back-to-back launches (HIP events on the launch stream); "
+                  f"median_ms: median of {n_time} single-launch event pairs",
     }
     if args.calibration_rows > 0:
         out["calibration"] = measure_calibration(B, W, w, stream, dev, args.calibration_rows,

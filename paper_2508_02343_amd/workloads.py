@@ -10,7 +10,7 @@ not available, so each configuration below stands in for them with the same
 layer shape, a heavy-tailed channel-outlier structure (a few channels scaled
 up, as in Fig. "motivation1", where outlier channels end up last after the
 reordering) and a split of roughly 5 bits per element with p4 > 50 %
-(Sec. 3.1 "FP4 dominance"; App. C.2 "5-5.6 bits").
+(Sec. 3.1 "FP4 dominance"; App. D.2 "5-5.6 bits").
 
 The permutation puts every regular channel first, in a seeded random order
 (what sorting the channel mean |X| of i.i.d. channels yields), and the
