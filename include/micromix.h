@@ -96,7 +96,7 @@
 extern "C" {
 #endif
 
-#define MM_ABI_VERSION 5
+#define MM_ABI_VERSION 6
 
 typedef enum {
   MM_OK = 0,
@@ -253,6 +253,29 @@ mm_status mm_calibrate_workspace_size(int64_t rows, int64_t K, int64_t* bytes);
 mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats,
                        void* workspace, int64_t workspace_bytes, int32_t* perm_out, int32_t* split_out,
                        void* stream);
+
+/*
+ * mm_calibrate without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  It computes exactly what mm_calibrate
+ * computes (same kernels, same results bit for bit), but its workspace is a
+ * library-owned static device array of 16 MiB (each GPU the library runs on
+ * holds one until the process ends).  The call allocates nothing: the
+ * array's device address is looked up once per device, on the first call
+ * made with that device current, and cached.
+ *   Limit: the plan for (rows, K) must fit the 16 MiB; every rows count fits
+ *   for K <= 31488.  Larger plans fail with MM_ERR_WORKSPACE before any work
+ *   is enqueued (mm_calibrate with a caller workspace takes them).
+ *   Sharing: every call on a GPU uses that GPU's one array.  Calls that
+ *   overlap in time on one GPU (other streams, other host threads) race on
+ *   it and give undefined results; calls ordered on one stream are safe.
+ *   No kernel reads the array before writing it, so what a previous call
+ *   left there does not matter.
+ * Arguments and errors as mm_calibrate's (no workspace, no workspace_bytes);
+ * MM_ERR_DEVICE also when the array's address cannot be looked up.
+ */
+mm_status mm_calibrate_no_alloc(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats,
+                                int32_t* perm_out, int32_t* split_out, void* stream);
 
 /* Static English name of a status code. */
 const char* mm_status_str(mm_status s);

@@ -17,6 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmicromix.so")
 
 MM_OK = 0
+ABI_VERSION = 6  # MM_ABI_VERSION of include/micromix.h this binding follows
 STATUS_NAMES = {0: "MM_OK", 1: "MM_ERR_NULL", 2: "MM_ERR_SHAPE", 3: "MM_ERR_SPLIT", 4: "MM_ERR_ALIGN",
                 5: "MM_ERR_FORMAT", 6: "MM_ERR_DEVICE", 7: "MM_ERR_WORKSPACE",
                 8: "MM_ERR_VALUE"}
@@ -78,6 +79,10 @@ def _load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mm_calibrate_workspace_size.restype = ctypes.c_int
     lib.mm_calibrate.argtypes = [P, I64, I64, I64, MMFormats, P, I64, P, P, P]
     lib.mm_calibrate.restype = ctypes.c_int
+    lib.mm_calibrate_no_alloc.argtypes = [P, I64, I64, I64, MMFormats, P, P, P]
+    lib.mm_calibrate_no_alloc.restype = ctypes.c_int
+    if lib.mm_abi_version() != ABI_VERSION:
+        raise ImportError(f"{path}: ABI version {lib.mm_abi_version()}, this binding needs {ABI_VERSION}")
     return lib
 
 
@@ -236,6 +241,25 @@ def calibrate_async(x: torch.Tensor, formats=DEFAULT_FORMATS, workspace: torch.T
     _check(lib.mm_calibrate(ctypes.c_void_p(x.data_ptr()), rows, K, x.stride(0), fm,
                             ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                             ctypes.c_void_p(perm.data_ptr()), ctypes.c_void_p(split.data_ptr()), _stream_ptr(stream)))
+    return perm, split
+
+
+def calibrate_no_alloc_async(x: torch.Tensor, perm: torch.Tensor, split: torch.Tensor, formats=DEFAULT_FORMATS,
+                             stream=None):
+    """mm_calibrate_no_alloc: mm_calibrate on the library's static scratch;
+    the caller supplies the outputs (perm int32 [K], split int32 [3]) and no
+    device memory is allocated anywhere in the call."""
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bfloat16 tensor")
+    rows, K = x.shape
+    if perm.dtype != torch.int32 or perm.numel() != K or not perm.is_contiguous() or perm.device != x.device:
+        raise ValueError("perm must be a contiguous int32 tensor of K elements on x's device")
+    if split.dtype != torch.int32 or split.numel() != 3 or not split.is_contiguous() or split.device != x.device:
+        raise ValueError("split must be a contiguous int32 tensor of 3 elements on x's device")
+    fm = MMFormats(FP6_FORMATS.get(formats[0], -1), FP8_FORMATS.get(formats[1], -1))
+    _check(lib.mm_calibrate_no_alloc(ctypes.c_void_p(x.data_ptr()), rows, K, x.stride(0), fm,
+                                     ctypes.c_void_p(perm.data_ptr()), ctypes.c_void_p(split.data_ptr()),
+                                     _stream_ptr(stream)))
     return perm, split
 
 

@@ -233,11 +233,14 @@ mm_status mm_calibrate_workspace_size(int64_t rows, int64_t K, int64_t* bytes) {
   return MM_OK;
 }
 
-mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats, void* workspace,
-                       int64_t workspace_bytes, int32_t* perm_out, int32_t* split_out, void* stream) {
-  g_err[0] = 0;
-  const char* who = "mm_calibrate";
-  if (!x_bf16 || !workspace || !perm_out || !split_out) return fail(MM_ERR_NULL, "%s: a pointer is NULL", who);
+namespace {
+
+// mm_calibrate and mm_calibrate_no_alloc: workspace == nullptr takes the
+// library's static scratch (looked up, never allocated).
+mm_status calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats, void* workspace,
+                    int64_t workspace_bytes, int32_t* perm_out, int32_t* split_out, void* stream, const char* who) {
+  const bool own = workspace == nullptr;
+  if (!x_bf16 || !perm_out || !split_out) return fail(MM_ERR_NULL, "%s: a pointer is NULL", who);
   mm_status st = check_calib_shape(rows, K, who);
   if (st != MM_OK) return st;
   if (ldx < K) return fail(MM_ERR_SHAPE, "%s: ld=%lld below K=%lld", who, (long long)ldx, (long long)K);
@@ -247,12 +250,20 @@ mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx,
   const CalibPlan p = calib_plan(rows, K);
   if ((int64_t)p.nchunks * p.tiles * 4 > kCalibHeaderBytes / 2 || 2 * ((K + 255) / 256) * 4 > kCalibHeaderBytes / 2)
     return fail(MM_ERR_SHAPE, "%s: internal plan exceeds the workspace header", who);
-  if (workspace_bytes < p.bytes)
+  if (own && p.bytes > mm::kCalibScratchBytes)
+    return fail(MM_ERR_WORKSPACE, "%s: rows=%lld, K=%lld need %lld bytes of workspace, beyond the %lld-byte static "
+                "scratch; call mm_calibrate with a workspace instead", who, (long long)rows, (long long)K,
+                (long long)p.bytes, (long long)mm::kCalibScratchBytes);
+  if (!own && workspace_bytes < p.bytes)
     return fail(MM_ERR_WORKSPACE, "%s: workspace of %lld bytes, %lld needed", who, (long long)workspace_bytes,
                 (long long)p.bytes);
   if (!aligned16(x_bf16) || ldx % 8 != 0) return fail(MM_ERR_ALIGN, "%s: input must be 16-byte aligned with ld %% 8 == 0", who);
-  if (!aligned16(workspace) || !aligned16(perm_out) || ((uintptr_t)split_out & 3u))
+  if ((!own && !aligned16(workspace)) || !aligned16(perm_out) || ((uintptr_t)split_out & 3u))
     return fail(MM_ERR_ALIGN, "%s: workspace and perm must be 16-byte aligned, split 4-byte aligned", who);
+  if (own) {
+    hipError_t e = mm::calibrate_scratch(&workspace);
+    if (e != hipSuccess) return fail(MM_ERR_DEVICE, "%s: static scratch lookup failed: %s", who, hipGetErrorString(e));
+  }
   mm::CalibArgs a;
   a.x = static_cast<const uint16_t*>(x_bf16);
   a.ldx = ldx;
@@ -273,6 +284,22 @@ mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx,
   hipError_t e = mm::launch_calibrate(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(MM_ERR_DEVICE, "%s: launch failed: %s", who, hipGetErrorString(e));
   return MM_OK;
+}
+
+}  // namespace
+
+mm_status mm_calibrate(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats, void* workspace,
+                       int64_t workspace_bytes, int32_t* perm_out, int32_t* split_out, void* stream) {
+  g_err[0] = 0;
+  if (!workspace) return fail(MM_ERR_NULL, "mm_calibrate: a pointer is NULL");
+  return calibrate(x_bf16, rows, K, ldx, formats, workspace, workspace_bytes, perm_out, split_out, stream,
+                   "mm_calibrate");
+}
+
+mm_status mm_calibrate_no_alloc(const void* x_bf16, int64_t rows, int64_t K, int64_t ldx, mm_formats formats,
+                                int32_t* perm_out, int32_t* split_out, void* stream) {
+  g_err[0] = 0;
+  return calibrate(x_bf16, rows, K, ldx, formats, nullptr, 0, perm_out, split_out, stream, "mm_calibrate_no_alloc");
 }
 
 mm_status mm_mx_layout_sizes(int64_t rows, int64_t K, mm_split split, mm_mx_sizes* out) {

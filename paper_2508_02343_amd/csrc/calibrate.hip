@@ -23,9 +23,19 @@
 //   4. place: rank[j] = the sum of j's slice counts, sigma[rank[j]] = j, and
 //      workgroup 0 sums the group counts into the split.
 // No atomics: every result is written by exactly one thread.
+#include <mutex>
+
 #include "kernels.hpp"
 
 namespace mm {
+
+// Workspace of mm_calibrate_no_alloc: every GPU the library runs on holds
+// its own copy.  In host code this name is only a stand-in for the symbol
+// (not a device address): kernels get the address calibrate_scratch()
+// looked up.  No kernel reads a workspace byte before writing it, so the
+// contents a previous call left need no clearing.
+static __device__ __align__(256) uint8_t scratch[kCalibScratchBytes];
+
 namespace {
 
 constexpr int kSumWaves = 4;               // waves per column-sum workgroup
@@ -217,6 +227,26 @@ __global__ __launch_bounds__(kRankThreads) void place_kernel(CalibArgs a) {
 }
 
 }  // namespace
+
+hipError_t calibrate_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || ((uintptr_t)p & 255u)) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_calibrate(const CalibArgs& a, hipStream_t stream) {
   const int tiles = (a.K + kTileCols - 1) / kTileCols;

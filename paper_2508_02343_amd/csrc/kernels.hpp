@@ -86,8 +86,18 @@ struct CalibArgs {
   int fp6_e2m3;        // T(6) with E2M3's constants instead of E3M2's
 };
 
+// Size of the library-owned calibration scratch (a static device array, one
+// per GPU, held until the process ends) that mm_calibrate_no_alloc uses in
+// place of a caller's workspace.  16 MiB covers every calibration plan up
+// to K = 31488 channels, whatever the number of rows.
+constexpr int64_t kCalibScratchBytes = 16ll << 20;
+
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream);
 hipError_t launch_calibrate(const CalibArgs& a, hipStream_t stream);
+// Device address of the current device's calibration scratch: looked up
+// with hipGetSymbolAddress on the first call on each device, with that
+// device current, and cached per device.  Allocates nothing.
+hipError_t calibrate_scratch(void** ptr);
 hipError_t launch_gemm_direct(const GemmArgs& a, hipStream_t stream);
 hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t stream);
 

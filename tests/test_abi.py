@@ -27,7 +27,7 @@ def _declared_functions():
 
 def test_header_declares_the_calls():
     names = _declared_functions()
-    for n in ("mm_quantize_act", "mm_quantize_weight", "mm_gemm", "mm_calibrate", "mm_calibrate_workspace_size",
+    for n in ("mm_quantize_act", "mm_quantize_weight", "mm_gemm", "mm_calibrate", "mm_calibrate_workspace_size", "mm_calibrate_no_alloc",
               "mm_rmsnorm_quantize_act",
               "mm_status_str", "mm_last_error", "mm_abi_version"):
         assert n in names
@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(b.LIB_PATH)
     for n in _declared_functions():
         assert hasattr(lib, n), n
-    assert b.lib.mm_abi_version() == 5
+    assert b.lib.mm_abi_version() == 6
 
 
 def test_status_strings():
@@ -259,3 +259,35 @@ def test_rmsnorm_quantize_rejects_bad_arguments():
     bad.formats = b.MMFormats(7, 0)
     assert _nq(bad) == "MM_ERR_FORMAT"
     assert b.lib.mm_last_error().decode()
+
+
+def _cal_na(rows=64, K=128, ldx=None, fm=(0, 0), x=FAKE, perm=FAKE, split=FAKE):
+    st = b.lib.mm_calibrate_no_alloc(ctypes.c_void_p(x), rows, K, ldx if ldx is not None else K, b.MMFormats(*fm),
+                                     ctypes.c_void_p(perm), ctypes.c_void_p(split), None)
+    return b.STATUS_NAMES[st]
+
+
+def test_calibrate_no_alloc_rejects_bad_arguments():
+    """The no-allocation variant validates like mm_calibrate, and rejects a
+    plan beyond its 16 MiB static scratch before touching the device."""
+    assert _cal_na(x=0) == "MM_ERR_NULL"
+    assert _cal_na(perm=0) == "MM_ERR_NULL"
+    assert _cal_na(split=0) == "MM_ERR_NULL"
+    assert _cal_na(rows=0) == "MM_ERR_SHAPE"
+    assert _cal_na(K=96 + 8) == "MM_ERR_SHAPE"
+    assert _cal_na(ldx=96) == "MM_ERR_SHAPE"
+    assert _cal_na(fm=(2, 0)) == "MM_ERR_FORMAT"
+    # the largest plan that fits: K = 31488 at any row count (reaches the alignment check)
+    st, n = _ws(1 << 20, 31488)
+    assert st == "MM_OK" and n <= 16 << 20
+    assert _cal_na(rows=1 << 20, K=31488, x=FAKE + 2) == "MM_ERR_ALIGN"
+    # one step wider no longer fits
+    st, n = _ws(1 << 20, 31520)
+    assert st == "MM_OK" and n > 16 << 20
+    assert _cal_na(rows=1 << 20, K=31520) == "MM_ERR_WORKSPACE"
+    msg = b.lib.mm_last_error().decode()
+    assert "static" in msg and str(16 << 20) in msg
+    assert _cal_na(rows=1 << 20, K=32768) == "MM_ERR_WORKSPACE"
+    assert _cal_na(x=FAKE + 2) == "MM_ERR_ALIGN"
+    assert _cal_na(perm=FAKE + 4) == "MM_ERR_ALIGN"
+    assert _cal_na(split=FAKE + 2) == "MM_ERR_ALIGN"
