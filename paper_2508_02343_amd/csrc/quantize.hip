@@ -3,7 +3,11 @@
 // sigma (Sec. 3.1), takes each 32-channel block's shared E8M0 scale and writes
 // E2M1 / E3M2 / E4M3 codes for the three groups (Sec. 2.1 MX rule).
 //
-// HBM-bound design for gfx950:
+// HBM-bound design for gfx950, two kernels:
+//  - the ring kernel (passes of two or more rows, K <= 8192, no norm; below
+//    the pipelined one): producer wavefronts load each pass straight into an
+//    LDS ring with global_load_lds_dwordx4, several passes in flight per CU;
+//  - the pipelined kernel, as follows.
 //  - a pass is `rpp` consecutive rows; the grid is sized to the number of
 //    workgroups the chip holds at once, each XCD takes a contiguous range of
 //    passes and its workgroups stride through it; one thread per (row,
@@ -96,17 +100,19 @@ __device__ __forceinline__ void zero_tail(const QuantArgs& a, int64_t step, int6
   for (int jj = j + 1; jj < kStepBlocks; ++jj) zero_block<G>(a, step, gstep, n, jj);
 }
 
-// Quantise block b (local to its group) of row n from LDS stage kStage; rows
-// past a.rows are padding and quantise an all-zero block.  The thread that
-// owns a group's last block also zeroes the padding blocks of that step.
-template <int kStage, bool kNorm>
-__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], int group, bool last, const QuantArgs& a,
-                                               int64_t n, int b, int gstep0, const uint32_t (&gpk)[16], float rn) {
+// Quantise block b (local to its group) of row n from the LDS stage at byte
+// offset `off` from the addresses; rows past a.rows are padding and quantise
+// an all-zero block.  The thread that owns a group's last block also zeroes
+// the padding blocks of that step.
+template <bool kNorm>
+__device__ __forceinline__ void quantize_block(const uint32_t (&addr)[32], uint32_t off, int group, bool last,
+                                               const QuantArgs& a, int64_t n, int b, int gstep0,
+                                               const uint32_t (&gpk)[16], float rn) {
   // gather: the block's 32 permuted channels, all reads issued before any
   // is used, then packed as 16 bf16 pairs
   uint16_t e[32];
 #pragma unroll
-  for (int i = 0; i < 32; ++i) e[i] = lds_u16(addr[i] + kStage * kStageOff);
+  for (int i = 0; i < 32; ++i) e[i] = lds_u16(addr[i] + off);
   __builtin_amdgcn_sched_barrier(0);
   uint32_t d[16];
   const bool pad_row = n >= a.rows;
@@ -412,15 +418,187 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
         for (int k = 0; k < 16; ++k) gq[k] = gpk[k];
       }
       if ((i & 1) == 0)
-        quantize_block<0, kNorm != 0>(addr, group, last, a, row, b, gstep0, gq, rn);
+        quantize_block<kNorm != 0>(addr, 0u, group, last, a, row, b, gstep0, gq, rn);
       else
-        quantize_block<1, kNorm != 0>(addr, group, last, a, row, b, gstep0, gq, rn);
+        quantize_block<kNorm != 0>(addr, (uint32_t)kStageOff, group, last, a, row, b, gstep0, gq, rn);
     }
     if (more) MM_STORE_PASS((i + 1) & 1);
     __syncthreads();
   }
 #undef MM_LOAD_PASS
 #undef MM_STORE_PASS
+}
+
+// ---------------------------------------------------------------------------
+// Ring variant (no RMSNorm, K <= 8192): one workgroup per CU, persistent over
+// a range of passes.  Four producer wavefronts move each pass's rows from HBM
+// straight into an LDS slot with global_load_lds_dwordx4 (1 KB per wavefront
+// instruction, no register staging); a ring of kRingSlots slots keeps up to
+// kRingSlots - 1 passes, about 96 KB per CU, in flight, where the pipelined
+// kernel above has at most one pass of register-staged loads per workgroup.
+// Eight consumer wavefronts quantise exactly as above (thread t owns
+// pass-row t / nblk and block t % nblk).  One s_barrier per pass hands a
+// landed slot to the consumers and the slot they have finished back to the
+// producers.  Only the producers load and only the consumers store, so each
+// producer's vmcnt counts its own loads alone and the wait for a pass is one
+// constant: every producer issues NPER loads for every pass (loads past the
+// pass's bytes repeat its last one, into the same LDS bytes).
+// ---------------------------------------------------------------------------
+constexpr int kRingSlots = 4;
+constexpr int kRingSlotMax = 32768;  // bytes of one pass's rows at most (a slot adds up to 1 KB of padding)
+constexpr int kProducerWaves = 4;
+constexpr int kConsumerWaves = 8;
+constexpr int kRingThreads = 64 * (kProducerWaves + kConsumerWaves);
+
+// vmcnt-only wait (expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the wait for loads in flight that __syncthreads
+// adds (the producers' loads must stay in flight across it).
+__device__ __forceinline__ void bare_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+__device__ __forceinline__ uint32_t uni32(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
+__device__ __forceinline__ const uint8_t* uni_ptr(const uint8_t* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return (const uint8_t*)(lo | (hi << 32));
+}
+
+// Direct global -> LDS load: lane i's 16 bytes at sbase + voff land at M0 +
+// 16 i.  Inline asm, so the compiler neither tracks nor waits for it; the
+// producers' explicit vmcnt waits do.  The s_nop covers the M0 write.
+__device__ __forceinline__ void dma16(uint32_t voff, const uint8_t* sbase, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase), "{m0}"(lds) : "memory");
+}
+
+template <int NPER>
+__global__ __launch_bounds__(kRingThreads, 1) void quantize_ring_kernel(QuantArgs a, int rpp, int row_stride,
+                                                                       int slot_stride) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t ring[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)ring;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int K = a.K;
+  const int nblk = K >> 5;
+  const int64_t passes = (a.rp + rpp - 1) / rpp;  // padding rows included
+
+  // this workgroup's passes: each XCD a contiguous range (the rows of a
+  // 32-row group share cache lines in the packed layout), its workgroups
+  // strided through it
+  int64_t q, q_end, stride;
+  if (gridDim.x % 8 == 0) {
+    const int x = blockIdx.x & 7;
+    q = passes * x / 8 + (blockIdx.x >> 3);
+    q_end = passes * (x + 1) / 8;
+    stride = gridDim.x / 8;
+  } else {
+    q = blockIdx.x;
+    q_end = passes;
+    stride = gridDim.x;
+  }
+  if (q >= q_end) return;  // uniform over the workgroup
+  const int64_t nk = (q_end - q + stride - 1) / stride;
+
+  if (wave >= kConsumerWaves) {
+    // producer: pass k goes to slot k % kRingSlots, row r of the pass at
+    // r * row_stride in the slot; wavefront pw issues the pass's 1 KB pieces
+    // pw, pw + 4, ... (a piece past the last repeats the last); passes past
+    // the workgroup's last repeat it
+    const int pw = wave - kConsumerWaves;
+    const int lane = tid & 63;
+    const int cpr = K >> 3;  // 16-byte chunks per row
+    // padded rows (row_stride > 2K, K a multiple of 512): whole 1 KB pieces
+    // per row; otherwise rows back to back, pieces across row ends
+    const bool padded = row_stride != 2 * K;
+    const int ipr = cpr >> 6;  // pieces per row when padded
+    const int nchunks = rpp * cpr;
+    const int ninstr = padded ? rpp * ipr : (nchunks + 63) >> 6;
+    auto issue = [&](int64_t k) {
+      const int64_t kk = k < nk ? k : nk - 1;
+      const int64_t r0 = (q + kk * stride) * rpp;
+      // rows past the input are read from its last row (their blocks
+      // quantise as padding and never use them)
+      const int64_t rb = r0 < a.rows ? r0 : a.rows - 1;
+      const uint8_t* base = uni_ptr(reinterpret_cast<const uint8_t*>(a.x + rb * a.ldx));
+      const uint32_t slot = lds0 + (uint32_t)(k % kRingSlots) * (uint32_t)slot_stride;
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) {
+        int i = pw + kProducerWaves * j;
+        i = i < ninstr ? i : ninstr - 1;
+        int rr, c;  // row within the pass, chunk within the row
+        uint32_t dst;
+        if (padded) {
+          rr = i / ipr;
+          const int ii = i - rr * ipr;
+          c = ii * 64 + lane;
+          dst = slot + (uint32_t)rr * (uint32_t)row_stride + (uint32_t)ii * 1024u;
+        } else {
+          int cc = i * 64 + lane;
+          cc = cc < nchunks ? cc : nchunks - 1;
+          rr = cc / cpr;
+          c = cc - rr * cpr;
+          dst = slot + (uint32_t)i * 1024u;
+        }
+        int64_t row = r0 + rr;
+        row = row < a.rows ? row : a.rows - 1;
+        const uint32_t voff = (uint32_t)((row - rb) * a.ldx * 2 + (int64_t)c * 16);
+        dma16(voff, base, uni32(dst));
+      }
+    };
+    for (int k = 0; k < kRingSlots - 1; ++k) issue(k);
+    for (int64_t k = 0; k < nk; ++k) {
+      // pass k landed (this wavefront's loads; the kRingSlots - 2 passes
+      // after it may still be in flight), then everyone's
+      wait_vmcnt<(kRingSlots - 2) * NPER>();
+      bare_barrier();
+      // the consumers are done with pass k - 1: refill its slot
+      issue(k + kRingSlots - 1);
+    }
+    wait_vmcnt<0>();  // no load may land after the workgroup's LDS is released
+    return;
+  }
+
+  // consumer: thread t owns block t / rpp of pass-row t % rpp, so the
+  // lanes that store one block's codes hold consecutive rows, whose codes
+  // are consecutive in the packed layout (one contiguous run per block
+  // instead of one 16-byte piece per lane); with padded rows those lanes'
+  // gather reads fall on different banks
+  const int blk = tid / rpp;
+  const int prow = tid - blk * rpp;
+  const bool active = blk < nblk;
+  uint32_t addr[32];
+  const uint32_t base = lds0 + (uint32_t)prow * (uint32_t)row_stride;
+#pragma unroll
+  for (int qq = 0; qq < 8; ++qq) {
+    const int4 v = *reinterpret_cast<const int4*>(a.perm + (active ? blk : 0) * 32 + 4 * qq);
+    const int p[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) addr[4 * qq + i] = base + 2u * (uint32_t)((unsigned)p[i] < (unsigned)K ? p[i] : 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 32; ++i) asm volatile("" : "+v"(addr[i]));
+  uint32_t gpk[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) gpk[i] = 0u;
+  const int bb = active ? blk : 0;
+  const int group = bb < a.nb[0] ? 0 : (bb < a.nb[0] + a.nb[1] ? 1 : 2);
+  const int b = bb - (group >= 1 ? a.nb[0] : 0) - (group >= 2 ? a.nb[1] : 0);
+  const int gstep0 = (group >= 1 ? a.steps[0] : 0) + (group >= 2 ? a.steps[1] : 0);
+  const bool last = b == (group == 0 ? a.nb[0] : (group == 1 ? a.nb[1] : a.nb[2])) - 1;
+  for (int64_t k = 0; k < nk; ++k) {
+    bare_barrier();
+    const int64_t row = (q + k * stride) * rpp + prow;
+    if (active && row < a.rp)
+      quantize_block<false>(addr, (uint32_t)(k % kRingSlots) * (uint32_t)slot_stride, group, last, a, row, b,
+                            gstep0, gpk, 0.0f);
+    // every read of this slot is done before the barrier that frees it
+    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));
+  }
 }
 
 // Allow more than 64 KB of dynamic LDS (two 32 KB stages plus the dummy
@@ -474,10 +652,81 @@ static hipError_t launch_pipelined(const QuantArgs& a, int rpp, int T, size_t ld
   return hipGetLastError();
 }
 
+// CUs of the current device (cached per thread for the last device).
+static hipError_t device_cus(int* cus) {
+  thread_local int last_dev = -1, last_cus = 0;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev != last_dev) {
+    e = hipDeviceGetAttribute(&last_cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    last_dev = dev;
+  }
+  *cus = last_cus;
+  return hipSuccess;
+}
+
+template <int NPER>
+static hipError_t launch_ring_n(const QuantArgs& a, int rpp, int row_stride, int slot_stride, int grid,
+                                hipStream_t stream) {
+  static bool attr = false;
+  const size_t lds = (size_t)kRingSlots * slot_stride;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(quantize_ring_kernel<NPER>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kRingSlots * (kRingSlotMax + 1024));
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL(quantize_ring_kernel<NPER>, dim3((unsigned)grid), dim3(kRingThreads), lds, stream, a, rpp,
+                     row_stride, slot_stride);
+  return hipGetLastError();
+}
+
+// The ring kernel for K <= 8192 without the norm; *used = false leaves the
+// launch to the kernels below.
+static hipError_t launch_ring(const QuantArgs& a, hipStream_t stream, bool* used) {
+  *used = false;
+  const int K = a.K;
+  const int nblk = K >> 5;
+  if (a.norm != 0 || nblk > 64 * kConsumerWaves || 2 * K > kRingSlotMax) return hipSuccess;
+  // rows per pass: as many as the consumer threads and one slot take
+  int rpp = 64 * kConsumerWaves / nblk;
+  if (rpp * 2 * K > kRingSlotMax) rpp = kRingSlotMax / (2 * K);
+  // one row per pass (K > 8192): the pipelined kernel, with two workgroups
+  // and twice the quantising wavefronts per CU, measured faster (K = 14336:
+  // 35 us against 42 us for 4096 rows)
+  if (rpp < 2) return hipSuccess;
+  // per-lane load offsets are 32-bit, relative to the pass's first row
+  if ((int64_t)rpp * a.ldx * 2 + (int64_t)K * 2 >= ((int64_t)1 << 32)) return hipSuccess;
+  // rows padded by 16 bytes in LDS when they are whole 1 KB loads (K a
+  // multiple of 512) and the pass has several, so the gather reads of one
+  // block's rows fall on different banks
+  const bool padded = K % 512 == 0 && rpp > 1;
+  const int row_stride = padded ? 2 * K + 16 : 2 * K;
+  const int bytes = rpp * row_stride;
+  const int slot_stride = (bytes + 1023) / 1024 * 1024;  // the last 1 KB load may run past the pass's bytes
+  const int ninstr = padded ? rpp * (2 * K / 1024) : (bytes + 1023) / 1024;
+  const int nper = (ninstr + kProducerWaves - 1) / kProducerWaves;
+  int cus = 0;
+  hipError_t e = device_cus(&cus);
+  if (e != hipSuccess) return e;
+  const int64_t passes = (a.rp + rpp - 1) / rpp;
+  const int grid = (int)(passes < cus ? passes : cus);
+  *used = true;
+  if (nper <= 1) return launch_ring_n<1>(a, rpp, row_stride, slot_stride, grid, stream);
+  if (nper <= 2) return launch_ring_n<2>(a, rpp, row_stride, slot_stride, grid, stream);
+  if (nper <= 4) return launch_ring_n<4>(a, rpp, row_stride, slot_stride, grid, stream);
+  return launch_ring_n<8>(a, rpp, row_stride, slot_stride, grid, stream);
+}
+
 static hipError_t launch_quantize_rows(const QuantArgs& a, hipStream_t stream) {
   const int K = a.K;
   const int nblk = K >> 5;
   const bool norm = a.norm != 0;
+  bool ring_used = false;
+  hipError_t re = launch_ring(a, stream, &ring_used);
+  if (re != hipSuccess || ring_used) return re;
   // A row wider than one stage (K > 16384) is quantised without overlap, one
   // row per workgroup of K/32 threads (up to 1024); with the norm its weights
   // follow the row, the dummy slot and the (row, part) sums in LDS.
