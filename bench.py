@@ -271,6 +271,30 @@ def launch_stats(stream, fn, n: int, mean_only: bool = False):
     return mean, med
 
 
+def norm_stats(B, W, ops, dev, stream, n: int, quant_ms: float) -> dict:
+    """The quantiser with the layer's RMSNorm fused in front (weight ~ 1 +
+    N(0, 0.25^2), eps 1e-5), against the unfused pair it replaces: torch's
+    bf16 RMSNorm pass (reads and writes the activation) then the plain
+    quantiser."""
+    import torch
+
+    w = ops.w
+    g_np = (1.0 + 0.25 * np.random.default_rng([w.seed, 9]).standard_normal(w.K)).astype(np.float32)
+    gamma = to_dev_bf16(W.f32_to_bf16_bits(g_np), dev)
+    fused_ms, fused_med = launch_stats(
+        stream, lambda i: B.rmsnorm_quantize_act(ops.X[i % ops.nbuf], gamma, 1e-5, ops.perm, w.split,
+                                                 out=ops.XQ[i % ops.nbuf], stream=stream), n)
+    xn = [torch.empty_like(ops.X[0]) for _ in range(min(ops.nbuf, 2))]
+    norm_ms = launch_stats(stream, lambda i: xn[i % len(xn)].copy_(torch.nn.functional.rms_norm(
+        ops.X[i % ops.nbuf], (w.K,), weight=gamma, eps=1e-5)), n, mean_only=True)
+    qbytes = quant_bytes(w.M, w.K, w.split) + 2 * w.K
+    return {"kernel": "RMSNorm fused with reorder-and-quantize", "ms": round(fused_ms, 5),
+            "median_ms": round(fused_med, 5), "achieved": round(qbytes / (fused_ms * 1e-3) / 1e9, 1),
+            "peak": PEAK_HBM, "unit": "GB/s", "frac": round(qbytes / (fused_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
+            "vs_plain_quantizer": round(fused_ms / quant_ms, 3),
+            "unfused_pair_ms": round(norm_ms + quant_ms, 5), "torch_rms_norm_ms": round(norm_ms, 5)}
+
+
 def gemm_roofline(w, mean_ms: float, median_ms: float) -> dict:
     """The GEMM against its roofline: the bit mix's MFMA peak for prefill
     shapes, HBM for the decode kernel (M <= 64)."""
@@ -354,12 +378,8 @@ def main() -> int:
     # each kernel alone, back to back over the same rotated buffers
     quant_ms, quant_med = launch_stats(stream, ops.quant, n_time)
     gemm_ms, gemm_med = launch_stats(stream, ops.gemm, n_time)
-    # the same quantiser with the layer's RMSNorm fused in front (weight ~ 1 + N(0, 0.25^2), eps 1e-5)
-    g_np = (1.0 + 0.25 * np.random.default_rng([w.seed, 9]).standard_normal(w.K)).astype(np.float32)
-    gamma = to_dev_bf16(W.f32_to_bf16_bits(g_np), dev)
-    norm_ms, norm_med = launch_stats(
-        stream, lambda i: B.rmsnorm_quantize_act(ops.X[i % ops.nbuf], gamma, 1e-5, ops.perm, w.split,
-                                                 out=ops.XQ[i % ops.nbuf], stream=stream), n_time)
+    # the same quantiser with the layer's RMSNorm fused in front
+    norm = norm_stats(B, W, ops, dev, stream, n_time, quant_ms)
 
     qkv = None
     if w.name == "llama8b_attn_2048x4096x4096" and not args.no_qkv:
@@ -391,10 +411,9 @@ def main() -> int:
     flops = 2.0 * w.M * w.N * w.K
     value = flops / (ms_per_step * 1e-3) / 1e12
     quant = quant_roofline(w, quant_ms, quant_med)
-    qbytes = quant["bytes_per_launch"]
     wq_gbps = quant_bytes(w.N, w.K, w.split) / (ops.wq_ms * 1e-3) / 1e9
 
-    def config_row(wl, q_mean, q_med, g_mean, g_med):
+    def config_row(wl, q_mean, q_med, g_mean, g_med, nrm):
         g = gemm_roofline(wl, g_mean, g_med)
         q = quant_roofline(wl, q_mean, q_med)
         return {"workload": wl.name, "M": wl.M, "K": wl.K, "N": wl.N, "split": list(wl.split),
@@ -402,7 +421,8 @@ def main() -> int:
                                            "mfma_util", "traffic") if k in g},
                 "quantizer": {k: q[k] for k in ("ms", "median_ms", "achieved", "unit", "frac")},
                 "quant_to_gemm_time": round(q_med / g_med, 4),
-                "quant_share_of_kernel_time": round(q_med / (q_med + g_med), 4)}
+                "quant_share_of_kernel_time": round(q_med / (q_med + g_med), 4),
+                "rmsnorm_quantizer": {k: nrm[k] for k in ("ms", "frac", "vs_plain_quantizer", "unfused_pair_ms")}}
 
     sweep = None
     if not args.no_sweep and w.M > DIRECT_MAX_M:
@@ -410,14 +430,14 @@ def main() -> int:
         sweep = []
         for wl in W.PREFILL:
             if wl.name == w.name:
-                sweep.append(config_row(wl, quant_ms, quant_med, gemm_ms, gemm_med))
+                sweep.append(config_row(wl, quant_ms, quant_med, gemm_ms, gemm_med, norm))
                 continue
             o2 = Operands(B, wl, dev, stream, args.min_working_set_mb)
             for i in range(args.warmup):
                 o2.step(i)
             q2 = launch_stats(stream, o2.quant, n_time)
             g2 = launch_stats(stream, o2.gemm, n_time)
-            sweep.append(config_row(wl, *q2, *g2))
+            sweep.append(config_row(wl, *q2, *g2, norm_stats(B, W, o2, dev, stream, n_time, q2[0])))
             del o2
             torch.cuda.empty_cache()
 
@@ -438,11 +458,7 @@ def main() -> int:
                    "x_dist": w.x_dist, "rotated_buffer_sets": ops.nbuf},
         "roofline": gemm_roofline(w, gemm_ms, gemm_med),
         "quantizer": quant,
-        "rmsnorm_quantizer": {"kernel": "RMSNorm fused with reorder-and-quantize", "ms": round(norm_ms, 5),
-                              "median_ms": round(norm_med, 5),
-                              "achieved": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM,
-                              "unit": "GB/s", "frac": round((qbytes + 2 * w.K) / (norm_ms * 1e-3) / 1e9 / PEAK_HBM, 4),
-                              "vs_plain_quantizer": round(norm_ms / quant_ms, 3)},
+        "rmsnorm_quantizer": norm,
         "gemm_ms": round(gemm_ms, 5),
         "quant_share_of_kernel_time": round(quant_med / (quant_med + gemm_med), 4),
         "prefill_configs": sweep,

@@ -4,9 +4,10 @@
 // E2M1 / E3M2 / E4M3 codes for the three groups (Sec. 2.1 MX rule).
 //
 // HBM-bound design for gfx950, two kernels:
-//  - the ring kernel (passes of two or more rows, K <= 8192, no norm; below
-//    the pipelined one): producer wavefronts load each pass straight into an
-//    LDS ring with global_load_lds_dwordx4, several passes in flight per CU;
+//  - the ring kernel (passes of two or more rows, K <= 8192; below the
+//    pipelined one): producer wavefronts load each pass straight into an
+//    LDS ring with global_load_lds_dwordx4, several passes in flight per CU,
+//    and with the norm also sum each pass's squares one pass ahead;
 //  - the pipelined kernel, as follows.
 //  - a pass is `rpp` consecutive rows; the grid is sized to the number of
 //    workgroups the chip holds at once, each XCD takes a contiguous range of
@@ -430,7 +431,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_rows_kernel(QuantArgs a,
 }
 
 // ---------------------------------------------------------------------------
-// Ring variant (no RMSNorm, K <= 8192): one workgroup per CU, persistent over
+// Ring variant (K <= 8192): one workgroup per CU, persistent over
 // a range of passes.  Four producer wavefronts move each pass's rows from HBM
 // straight into an LDS slot with global_load_lds_dwordx4 (1 KB per wavefront
 // instruction, no register staging); a ring of kRingSlots slots keeps up to
@@ -449,6 +450,7 @@ constexpr int kRingSlotMax = 32768;  // bytes of one pass's rows at most (a slot
 constexpr int kProducerWaves = 4;
 constexpr int kConsumerWaves = 8;
 constexpr int kRingThreads = 64 * (kProducerWaves + kConsumerWaves);
+constexpr int kMaxRingRows = 64 * kConsumerWaves;  // rows per pass at most (one block per row)
 
 // vmcnt-only wait (expcnt and lgkmcnt left at their maxima).
 template <int N>
@@ -476,11 +478,42 @@ __device__ __forceinline__ void dma16(uint32_t voff, const uint8_t* sbase, uint3
   asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase), "{m0}"(lds) : "memory");
 }
 
-template <int NPER>
+// Square sums of the rows of the pass in the slot at `slot` (row r at r *
+// row_stride), one row per producer wavefront at a time, into the fp64
+// words at `sums`: four accumulators per lane over 16-byte reads, then a
+// fixed shuffle tree, so the result does not depend on timing (squares of
+// bf16 values are exact in fp64).
+__device__ __forceinline__ void ring_row_sums(uint32_t slot, int row_stride, int rpp, int K, int pw, int lane,
+                                              uint32_t sums) {
+  for (int r = pw; r < rpp; r += kProducerWaves) {
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int c = lane; c < (K >> 3); c += 64) {
+      const u32x4 v = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(
+          (uintptr_t)(slot + (uint32_t)r * (uint32_t)row_stride + (uint32_t)c * 16u));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const double lo = (double)__uint_as_float(v[k] << 16), hi = (double)__uint_as_float(v[k] & 0xFFFF0000u);
+        acc[k] += lo * lo;
+        acc[k] += hi * hi;
+      }
+    }
+    double t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
+    if (lane == 0) *reinterpret_cast<__attribute__((address_space(3))) double*>((uintptr_t)(sums + 8u * r)) = t;
+  }
+}
+
+// kNorm: the RMSNorm in front.  The producers then also sum each pass's
+// squares one pass ahead (after the barrier at which pass k + 1 has landed,
+// into one of two sum buffers), so the consumers of pass k find its row
+// factors ready; this keeps one pass fewer in flight.
+template <int NPER, bool kNorm>
 __global__ __launch_bounds__(kRingThreads, 1) void quantize_ring_kernel(QuantArgs a, int rpp, int row_stride,
                                                                        int slot_stride) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t ring[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)ring;
+  // the norm's row square sums: two buffers of kMaxRingRows fp64 words after the slots
+  const uint32_t sums0 = lds0 + (uint32_t)kRingSlots * (uint32_t)slot_stride;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int K = a.K;
@@ -551,13 +584,24 @@ __global__ __launch_bounds__(kRingThreads, 1) void quantize_ring_kernel(QuantArg
       }
     };
     for (int k = 0; k < kRingSlots - 1; ++k) issue(k);
+    if constexpr (kNorm) {
+      // the sums of pass 0 before the consumers start
+      wait_vmcnt<(kRingSlots - 2) * NPER>();
+      bare_barrier();
+      ring_row_sums(lds0, row_stride, rpp, K, pw, lane, sums0);
+    }
     for (int64_t k = 0; k < nk; ++k) {
       // pass k landed (this wavefront's loads; the kRingSlots - 2 passes
-      // after it may still be in flight), then everyone's
-      wait_vmcnt<(kRingSlots - 2) * NPER>();
+      // after it may still be in flight), then everyone's; with the norm
+      // pass k + 1 too, whose sums follow
+      wait_vmcnt<(kRingSlots - (kNorm ? 3 : 2)) * NPER>();
       bare_barrier();
       // the consumers are done with pass k - 1: refill its slot
       issue(k + kRingSlots - 1);
+      if constexpr (kNorm)
+        if (k + 1 < nk)
+          ring_row_sums(lds0 + (uint32_t)((k + 1) % kRingSlots) * (uint32_t)slot_stride, row_stride, rpp, K, pw,
+                        lane, sums0 + (uint32_t)((k + 1) & 1) * 8u * kMaxRingRows);
     }
     wait_vmcnt<0>();  // no load may land after the workgroup's LDS is released
     return;
@@ -582,20 +626,42 @@ __global__ __launch_bounds__(kRingThreads, 1) void quantize_ring_kernel(QuantArg
   }
 #pragma unroll
   for (int i = 0; i < 32; ++i) asm volatile("" : "+v"(addr[i]));
+  // the norm weights of this thread's block, gathered by sigma, as bf16 pairs
   uint32_t gpk[16];
+  if constexpr (kNorm) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) gpk[i] = 0u;
+    for (int qq = 0; qq < 8; ++qq) {
+      const int4 v = *reinterpret_cast<const int4*>(a.perm + (active ? blk : 0) * 32 + 4 * qq);
+      const int p[4] = {v.x, v.y, v.z, v.w};
+      uint32_t gg[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gg[i] = a.gamma[(unsigned)p[i] < (unsigned)K ? p[i] : 0];
+      gpk[2 * qq] = gg[0] | (gg[1] << 16);
+      gpk[2 * qq + 1] = gg[2] | (gg[3] << 16);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) gpk[i] = 0u;
+  }
   const int bb = active ? blk : 0;
   const int group = bb < a.nb[0] ? 0 : (bb < a.nb[0] + a.nb[1] ? 1 : 2);
   const int b = bb - (group >= 1 ? a.nb[0] : 0) - (group >= 2 ? a.nb[1] : 0);
   const int gstep0 = (group >= 1 ? a.steps[0] : 0) + (group >= 2 ? a.steps[1] : 0);
   const bool last = b == (group == 0 ? a.nb[0] : (group == 1 ? a.nb[1] : a.nb[2])) - 1;
+  if constexpr (kNorm) bare_barrier();  // the producers' barrier before pass 0's sums
   for (int64_t k = 0; k < nk; ++k) {
     bare_barrier();
     const int64_t row = (q + k * stride) * rpp + prow;
+    float rn = 0.0f;
+    if constexpr (kNorm) {
+      // fp32(1 / sqrt(mean(x^2) + eps)) from the row's fp64 square sum
+      const double sq = *reinterpret_cast<const __attribute__((address_space(3))) double*>(
+          (uintptr_t)(sums0 + (uint32_t)(k & 1) * 8u * kMaxRingRows + 8u * (uint32_t)prow));
+      rn = (float)(1.0 / sqrt(sq / (double)K + (double)a.eps));
+    }
     if (active && row < a.rp)
-      quantize_block<false>(addr, (uint32_t)(k % kRingSlots) * (uint32_t)slot_stride, group, last, a, row, b,
-                            gstep0, gpk, 0.0f);
+      quantize_block<kNorm>(addr, (uint32_t)(k % kRingSlots) * (uint32_t)slot_stride, group, last, a, row, b,
+                            gstep0, gpk, rn);
     // every read of this slot is done before the barrier that frees it
     __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));
   }
@@ -667,29 +733,40 @@ static hipError_t device_cus(int* cus) {
   return hipSuccess;
 }
 
-template <int NPER>
+template <int NPER, bool kNorm>
 static hipError_t launch_ring_n(const QuantArgs& a, int rpp, int row_stride, int slot_stride, int grid,
                                 hipStream_t stream) {
   static bool attr = false;
-  const size_t lds = (size_t)kRingSlots * slot_stride;
+  constexpr size_t kSumBytes = 2 * 8 * kMaxRingRows;
+  const size_t lds = (size_t)kRingSlots * slot_stride + (kNorm ? kSumBytes : 0);
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(quantize_ring_kernel<NPER>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kRingSlots * (kRingSlotMax + 1024));
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(quantize_ring_kernel<NPER, kNorm>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       kRingSlots * (kRingSlotMax + 1024) + kSumBytes);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  hipLaunchKernelGGL(quantize_ring_kernel<NPER>, dim3((unsigned)grid), dim3(kRingThreads), lds, stream, a, rpp,
-                     row_stride, slot_stride);
+  hipLaunchKernelGGL((quantize_ring_kernel<NPER, kNorm>), dim3((unsigned)grid), dim3(kRingThreads), lds, stream, a,
+                     rpp, row_stride, slot_stride);
   return hipGetLastError();
 }
 
-// The ring kernel for K <= 8192 without the norm; *used = false leaves the
-// launch to the kernels below.
+template <bool kNorm>
+static hipError_t launch_ring_norm(const QuantArgs& a, int nper, int rpp, int row_stride, int slot_stride, int grid,
+                                   hipStream_t stream) {
+  if (nper <= 1) return launch_ring_n<1, kNorm>(a, rpp, row_stride, slot_stride, grid, stream);
+  if (nper <= 2) return launch_ring_n<2, kNorm>(a, rpp, row_stride, slot_stride, grid, stream);
+  if (nper <= 4) return launch_ring_n<4, kNorm>(a, rpp, row_stride, slot_stride, grid, stream);
+  return launch_ring_n<8, kNorm>(a, rpp, row_stride, slot_stride, grid, stream);
+}
+
+// The ring kernel for K <= 8192 (passes of two or more rows), with or
+// without the norm; *used = false leaves the launch to the kernels below.
 static hipError_t launch_ring(const QuantArgs& a, hipStream_t stream, bool* used) {
   *used = false;
   const int K = a.K;
   const int nblk = K >> 5;
-  if (a.norm != 0 || nblk > 64 * kConsumerWaves || 2 * K > kRingSlotMax) return hipSuccess;
+  if (nblk > 64 * kConsumerWaves || 2 * K > kRingSlotMax) return hipSuccess;
   // rows per pass: as many as the consumer threads and one slot take
   int rpp = 64 * kConsumerWaves / nblk;
   if (rpp * 2 * K > kRingSlotMax) rpp = kRingSlotMax / (2 * K);
@@ -714,10 +791,8 @@ static hipError_t launch_ring(const QuantArgs& a, hipStream_t stream, bool* used
   const int64_t passes = (a.rp + rpp - 1) / rpp;
   const int grid = (int)(passes < cus ? passes : cus);
   *used = true;
-  if (nper <= 1) return launch_ring_n<1>(a, rpp, row_stride, slot_stride, grid, stream);
-  if (nper <= 2) return launch_ring_n<2>(a, rpp, row_stride, slot_stride, grid, stream);
-  if (nper <= 4) return launch_ring_n<4>(a, rpp, row_stride, slot_stride, grid, stream);
-  return launch_ring_n<8>(a, rpp, row_stride, slot_stride, grid, stream);
+  if (a.norm != 0) return launch_ring_norm<true>(a, nper, rpp, row_stride, slot_stride, grid, stream);
+  return launch_ring_norm<false>(a, nper, rpp, row_stride, slot_stride, grid, stream);
 }
 
 static hipError_t launch_quantize_rows(const QuantArgs& a, hipStream_t stream) {
