@@ -163,14 +163,33 @@ class MXTensor:
                 for k in ("q4", "q6", "q8", "sc")}
 
 
+def _check_mx(t: MXTensor, rows: int, K: int, split, device, name: str) -> None:
+    """An MXTensor whose buffers hold the packed layout of (rows, K, split)
+    on `device` (the library reads and writes exactly those bytes)."""
+    if t.rows != rows or t.K != K or tuple(int(p) for p in t.split) != tuple(int(p) for p in split):
+        raise ValueError(f"{name} is [{t.rows}, {t.K}] split {tuple(t.split)}, expected [{rows}, {K}] split "
+                         f"{tuple(split)}")
+    sz = layout_sizes(rows, K, split)
+    for b in ("q4", "q6", "q8", "sc"):
+        buf = getattr(t, b)
+        n = 0 if buf is None else buf.numel() * buf.element_size()
+        if n < sz[b]:
+            raise ValueError(f"{name}.{b} holds {n} bytes, the layout needs {sz[b]}")
+        if buf is not None and (buf.device != device or not buf.is_contiguous()):
+            raise ValueError(f"{name}.{b} must be contiguous and on {device}")
+
+
 def _quantize(fn, x: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | None, stream, formats) -> MXTensor:
-    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
-        raise ValueError("x must be a 2-D row-major bfloat16 tensor")
-    if perm.dtype != torch.int32 or not perm.is_contiguous():
-        raise ValueError("perm must be a contiguous int32 tensor")
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
+        raise ValueError("x must be a 2-D row-major bfloat16 device tensor")
     rows, K = x.shape
+    if perm.dtype != torch.int32 or not perm.is_contiguous() or perm.numel() != K or perm.device != x.device:
+        raise ValueError("perm must be a contiguous int32 tensor of K elements on x's device")
+    split = tuple(int(p) for p in split)
     if out is None:
         out = MXTensor.empty(rows, K, split, device=x.device, formats=formats)
+    else:
+        _check_mx(out, rows, K, split, x.device, "out")
     d = out.descriptor()
     _check(fn(ctypes.c_void_p(x.data_ptr()), x.stride(0), ctypes.c_void_p(perm.data_ptr()), ctypes.byref(d),
               _stream_ptr(stream)))
@@ -207,9 +226,15 @@ def quantize_weight(w: torch.Tensor, perm: torch.Tensor, split, out: MXTensor | 
 
 def gemm(a: MXTensor, w: MXTensor, y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """mm_gemm: Y[M, N] = A W^T in bf16 (one fp32 accumulator over all groups)."""
+    dev = a.sc.device
+    _check_mx(a, a.rows, a.K, a.split, dev, "a")
+    _check_mx(w, w.rows, w.K, w.split, dev, "w")
     if y is None:
         ldy = _round16(w.rows) if w.rows % 8 else w.rows
-        y = torch.empty((a.rows, ldy), dtype=torch.bfloat16, device=a.sc.device)[:, : w.rows]
+        y = torch.empty((a.rows, ldy), dtype=torch.bfloat16, device=dev)[:, : w.rows]
+    elif (y.dtype != torch.bfloat16 or y.dim() != 2 or tuple(y.shape) != (a.rows, w.rows) or y.stride(1) != 1
+          or y.device != dev):
+        raise ValueError(f"y must be a bfloat16 [{a.rows}, {w.rows}] tensor with unit column stride on {dev}")
     da, dw = a.descriptor(), w.descriptor()
     _check(lib.mm_gemm(ctypes.byref(da), ctypes.byref(dw), ctypes.c_void_p(y.data_ptr()), y.stride(0),
                        _stream_ptr(stream)))
