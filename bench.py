@@ -233,17 +233,34 @@ class Operands:
             B.quantize_act(self.X[k], self.perm, w.split, out=self.XQ[k], stream=stream)
         torch.cuda.synchronize()
 
-    def quant(self, i):
+    def quant(self, i, stream=None):
         k = i % self.nbuf
-        self.B.quantize_act(self.X[k], self.perm, self.w.split, out=self.XQ[k], stream=self.stream)
+        self.B.quantize_act(self.X[k], self.perm, self.w.split, out=self.XQ[k], stream=stream or self.stream)
 
-    def gemm(self, i):
+    def gemm(self, i, stream=None):
         k = i % self.nbuf
-        self.B.gemm(self.XQ[k], self.WQ[k], y=self.Y[k], stream=self.stream)
+        self.B.gemm(self.XQ[k], self.WQ[k], y=self.Y[k], stream=stream or self.stream)
 
-    def step(self, i):
-        self.quant(i)
-        self.gemm(i)
+    def step(self, i, stream=None):
+        self.quant(i, stream)
+        self.gemm(i, stream)
+
+
+def capture_steps(ops, n: int, stream):
+    """A HIP graph of steps 0 .. n-1 (the launches only; the Python and
+    ctypes cost of issuing 2 n kernels one by one is paid once, at capture)."""
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        cs = torch.cuda.current_stream()
+        for i in range(n):
+            ops.step(i, cs)
+    torch.cuda.synchronize()
+    return graph
 
 
 def to_dev_bf16(bits, dev):
@@ -391,11 +408,28 @@ def main() -> int:
     for i in range(args.warmup):
         ops.step(i)
     torch.cuda.synchronize()
+    # the same K steps issued one by one (host launch cost included) ...
     t0 = time.perf_counter()
     for i in range(args.steps):
         ops.step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    eager_ms = (t1 - t0) * 1e3 / args.steps
+    ref_y = [y.clone() for y in ops.Y]
+    # ... and as one replay of a captured graph of exactly K steps, the timed
+    # figure; every replay's outputs must equal the eager ones bit for bit
+    graph = capture_steps(ops, args.steps, stream)
+    graph.replay()
+    torch.cuda.synchronize()
+    graph_ok = all(torch.equal(a, b) for a, b in zip(ops.Y, ref_y))
+    t0 = time.perf_counter()
+    graph.replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    graph_ok = graph_ok and all(torch.equal(a, b) for a, b in zip(ops.Y, ref_y))
+    if not graph_ok:
+        raise RuntimeError("graph replay of the steps differs from their eager launches")
+    del graph, ref_y
 
     # each kernel alone, back to back over the same rotated buffers
     quant_ms, quant_med = launch_stats(stream, ops.quant, n_time)
@@ -486,8 +520,11 @@ def main() -> int:
         "prefill_configs": sweep,
         "shared_activation_qkv": qkv,
         "weight_quantize": {"ms": round(ops.wq_ms, 5), "GB/s": round(wq_gbps, 1)},
-        "timing": f"per-kernel ms: mean of {n_time} back-to-back launches (HIP events on the launch stream); "
-                  f"median_ms: median of {n_time} single-launch event pairs",
+        "timing": f"ms_per_step: one replay of a HIP graph of the {args.steps} steps (outputs checked equal to "
+                  f"their eager launches), wall clock between synchronizations; per-kernel ms: mean of "
+                  f"{n_time} back-to-back launches (HIP events on the launch stream); median_ms: median of "
+                  f"{n_time} single-launch event pairs",
+        "ms_per_step_eager": round(eager_ms, 5),
     }
     if args.calibration_rows > 0:
         out["calibration"] = measure_calibration(B, W, w, stream, dev, args.calibration_rows,
