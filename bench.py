@@ -176,8 +176,8 @@ def cpu_baseline(w, seconds: float) -> dict:
 
 def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps: int = 10) -> dict:
     """mm_calibrate over `rows` calibration tokens of the layer's width K
-    (offline, not part of the step): whole-call time with HIP events on the
-    launch stream, and HBM bandwidth over the bytes it must move (X read once,
+    (offline, not part of the step): whole-call time (a graph of `reps`
+    calls, HIP events around its replays), and HBM bandwidth over the bytes it must move (X read once,
     sigma and the split written)."""
     import torch
 
@@ -191,13 +191,10 @@ def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps
     split = torch.empty(3, dtype=torch.int32, device=dev)
     for i in range(2):
         B.calibrate_async(xs[i % nset], workspace=ws, perm=perm, split=split, stream=stream)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for i in range(reps):
-        B.calibrate_async(xs[i % nset], workspace=ws, perm=perm, split=split, stream=stream)
-    e1.record(stream)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    # its launches captured as a graph of `reps` calls (no host time between them)
+    ms = launch_stats(stream, lambda i, s: B.calibrate_async(xs[i % nset], workspace=ws, perm=perm, split=split,
+                                                             stream=s), reps, mean_only=True)
     nbytes = rows * w.K * 2 + w.K * 4 + 12
     gbps = nbytes / (ms * 1e-3) / 1e9
     return {"kernel": "offline calibration (mm_calibrate, 4 launches)", "rows": rows, "K": w.K, "ms": round(ms, 5),
@@ -208,7 +205,10 @@ def measure_calibration(B, W, w, stream, dev, rows: int, min_set_mb: float, reps
 class Operands:
     """One workload's device buffers: bf16 activations, their packed
     quantised form, the packed (offline-quantised) weight and the bf16
-    output, in several sets rotated so the working set exceeds the cache."""
+    output, in several sets rotated so that what each kernel touches over a
+    rotation (the quantiser: activations and their codes; the GEMM: codes,
+    weight and output) exceeds min_set_mb, well past the 256 MB Infinity
+    Cache: every launch reads its inputs from HBM."""
 
     def __init__(self, B, w, dev, stream, min_set_mb: float):
         import torch
@@ -220,15 +220,19 @@ class Operands:
         del xb, wb
         p4, p6, p8 = w.split
         row = p4 // 2 + 3 * p6 // 4 + p8 + w.K // 32
-        set_bytes = w.M * w.K * 2 + w.M * row + w.N * row + w.M * w.N * 2
-        self.nbuf = n = max(1, int(np.ceil(min_set_mb * 1e6 / set_bytes)))
+        quant_set = w.M * w.K * 2 + w.M * row
+        gemm_set = w.M * row + w.N * row + w.M * w.N * 2
+        # (a decode step's activation is a few KB, read from cache whatever
+        # the rotation: there the GEMM's weight stream sets the count)
+        touched = min(quant_set, gemm_set) if w.M > DIRECT_MAX_M else gemm_set
+        self.nbuf = n = max(1, int(np.ceil(min_set_mb * 1e6 / touched)))
         self.X = [x0] + [x0.clone() for _ in range(n - 1)]
         self.XQ = [B.MXTensor.empty(w.M, w.K, w.split, device=dev) for _ in range(n)]
         self.WQ = [B.MXTensor.empty(w.N, w.K, w.split, device=dev) for _ in range(n)]
         self.Y = [torch.empty((w.M, w.N), dtype=torch.bfloat16, device=dev) for _ in range(n)]
         # offline weight quantisation (once per weight), timed on its own
-        self.wq_ms = launch_stats(stream, lambda i: B.quantize_weight(w0, self.perm, w.split, out=self.WQ[i],
-                                                                      stream=stream), n, mean_only=True)
+        self.wq_ms = launch_stats(stream, lambda i, s: B.quantize_weight(w0, self.perm, w.split, out=self.WQ[i],
+                                                                         stream=s), n, mean_only=True)
         for k in range(n):
             B.quantize_act(self.X[k], self.perm, w.split, out=self.XQ[k], stream=stream)
         torch.cuda.synchronize()
@@ -249,6 +253,18 @@ class Operands:
 def capture_steps(ops, n: int, stream):
     """A HIP graph of steps 0 .. n-1 (the launches only; the Python and
     ctypes cost of issuing 2 n kernels one by one is paid once, at capture)."""
+    return graph_of(ops.step, n, stream)
+
+
+def to_dev_bf16(bits, dev):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
+def graph_of(fn, n: int, stream):
+    """A HIP graph of fn(0, s) .. fn(n-1, s), s the capture stream (the
+    launches only: no host time between them when it is replayed)."""
     import torch
 
     side = torch.cuda.Stream()
@@ -258,42 +274,43 @@ def capture_steps(ops, n: int, stream):
     with torch.cuda.graph(graph, stream=side):
         cs = torch.cuda.current_stream()
         for i in range(n):
-            ops.step(i, cs)
+            fn(i, cs)
     torch.cuda.synchronize()
     return graph
 
 
-def to_dev_bf16(bits, dev):
+def replay_ms(graph, stream, reps: int) -> list:
+    """Durations of `reps` replays of a graph, from HIP events recorded on
+    the stream it is replayed on."""
     import torch
 
-    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+    out = []
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            graph.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1))
+    return out
 
 
-def launch_stats(stream, fn, n: int, mean_only: bool = False):
-    """Launch durations of fn(0..n-1) on `stream`, from HIP events recorded
-    on that stream.  The mean comes from n back-to-back launches with one
-    event pair around all of them (what a kernel trace averages); the median
-    from a second pass with an event after every launch.  Returns (mean ms,
-    median ms), or the mean alone."""
-    import torch
-
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for i in range(n):
-        fn(i)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    mean = e0.elapsed_time(e1) / n
+def launch_stats(stream, fn, n: int, mean_only: bool = False, reps: int = 5):
+    """Launch durations of fn(i, s), i = 0..n-1, s the stream to launch on:
+    the n launches are captured as one HIP graph, so host issue time (ctypes,
+    Python) never leaves the GPU idle between them, and the graph is
+    replayed `reps` times after one untimed replay.  mean: all replays'
+    time over reps * n launches; median: the median of the replays' per-launch
+    means.  Returns (mean ms, median ms), or the mean alone."""
+    graph = graph_of(fn, n, stream)
+    replay_ms(graph, stream, 1)
+    t = replay_ms(graph, stream, reps)
+    del graph
+    mean = sum(t) / (reps * n)
     if mean_only:
         return mean
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-    ev[0].record(stream)
-    for i in range(n):
-        fn(i)
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    med = float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]))
-    return mean, med
+    return mean, float(np.median(t)) / n
 
 
 def norm_stats(B, W, ops, dev, stream, n: int, quant_ms: float) -> dict:
@@ -307,8 +324,8 @@ def norm_stats(B, W, ops, dev, stream, n: int, quant_ms: float) -> dict:
     g_np = (1.0 + 0.25 * np.random.default_rng([w.seed, 9]).standard_normal(w.K)).astype(np.float32)
     gamma = to_dev_bf16(W.f32_to_bf16_bits(g_np), dev)
     fused_ms, fused_med = launch_stats(
-        stream, lambda i: B.rmsnorm_quantize_act(ops.X[i % ops.nbuf], gamma, 1e-5, ops.perm, w.split,
-                                                 out=ops.XQ[i % ops.nbuf], stream=stream), n)
+        stream, lambda i, s: B.rmsnorm_quantize_act(ops.X[i % ops.nbuf], gamma, 1e-5, ops.perm, w.split,
+                                                    out=ops.XQ[i % ops.nbuf], stream=s), n)
     # torch's norm is timed as a captured graph of 20 calls (its Python
     # dispatch per call is slower than the kernel itself)
     reps = 20
@@ -324,7 +341,7 @@ def norm_stats(B, W, ops, dev, stream, n: int, quant_ms: float) -> dict:
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         outs = [torch.nn.functional.rms_norm(x, (w.K,), weight=gamma, eps=1e-5) for x in xs]
-    norm_ms = launch_stats(stream, lambda i: graph.replay(), max(3, n // reps), mean_only=True) / reps
+    norm_ms = float(np.mean(replay_ms(graph, stream, max(3, n // reps)))) / reps
     del graph, outs
     qbytes = quant_bytes(w.M, w.K, w.split) + 2 * w.K
     return {"kernel": "RMSNorm fused with reorder-and-quantize", "ms": round(fused_ms, 5),
@@ -449,12 +466,12 @@ def main() -> int:
         wsep = [B.quantize_weight(to_dev_bf16(x, dev), ops.perm, w.split, stream=stream) for x in wl]
         yst = torch.empty((w.M, sum(parts)), dtype=torch.bfloat16, device=dev)
         ysep = [torch.empty((w.M, n), dtype=torch.bfloat16, device=dev) for n in parts]
-        st_ms = launch_stats(stream, lambda i: B.gemm(ops.XQ[i % ops.nbuf], wst, y=yst, stream=stream), n_time,
+        st_ms = launch_stats(stream, lambda i, s: B.gemm(ops.XQ[i % ops.nbuf], wst, y=yst, stream=s), n_time,
                              mean_only=True)
 
-        def three(i):
+        def three(i, s):
             for k in range(3):
-                B.gemm(ops.XQ[i % ops.nbuf], wsep[k], y=ysep[k], stream=stream)
+                B.gemm(ops.XQ[i % ops.nbuf], wsep[k], y=ysep[k], stream=s)
 
         sep_ms = launch_stats(stream, three, n_time, mean_only=True)
         qflops = 2.0 * w.M * w.K * sum(parts)
@@ -521,9 +538,9 @@ def main() -> int:
         "shared_activation_qkv": qkv,
         "weight_quantize": {"ms": round(ops.wq_ms, 5), "GB/s": round(wq_gbps, 1)},
         "timing": f"ms_per_step: one replay of a HIP graph of the {args.steps} steps (outputs checked equal to "
-                  f"their eager launches), wall clock between synchronizations; per-kernel ms: mean of "
-                  f"{n_time} back-to-back launches (HIP events on the launch stream); median_ms: median of "
-                  f"{n_time} single-launch event pairs",
+                  f"their eager launches), wall clock between synchronizations; per-kernel ms: a HIP graph of "
+                  f"{n_time} launches replayed 5 times (HIP events around each replay), mean over all launches; "
+                  f"median_ms: median of the replays' per-launch means",
         "ms_per_step_eager": round(eager_ms, 5),
     }
     if args.calibration_rows > 0:
