@@ -121,6 +121,16 @@ def test_layer_widths(w, eps):
     _check(w.x_bits(rows), _gamma(w.K, 1), eps, w.perm(), w.split, ctx=w.name)
 
 
+@pytest.mark.parametrize("rows", [3, 300])
+def test_one_row_per_pass(rows):
+    # 8192 < K <= 16384: one row per pass through the two-stage pipelined
+    # kernel (K = 14336, the Llama-3-8B MLP width), ragged row counts
+    K, split = 14336, (10752, 2688, 896)
+    rng = np.random.default_rng(rows + 14)
+    x = (rng.standard_normal((rows, K)) * np.exp(rng.normal(0, 1, K))).astype(np.float32)
+    _check(f32_bits(x), _gamma(K, rows), 1e-5, rng.permutation(K).astype(np.int32), split, ctx=f"K14336 rows{rows}")
+
+
 def test_wide_rows_one_per_workgroup():
     # K above one LDS stage: the one-row-per-workgroup kernel
     K, split = 28672, (20480, 4096, 4096)
