@@ -30,7 +30,12 @@
 // The vmcnt wait for a stage is then one constant, and issuing the next
 // stage is a loop-carried cursor (one base pointer per wavefront, per-lane
 // offsets fixed per group) instead of per-stage address arithmetic, which
-// a single wavefront per SIMD could not hide behind its MFMAs.
+// a single wavefront per SIMD could not hide behind its MFMAs.  The K loop
+// runs in segments whose refills stay in one group: inside a segment the
+// cursor only adds a precomputed increment (no branch, its per-lane offsets
+// untouched), and it is re-pointed between segments; with the group change
+// tested every stage, the scalar bookkeeping of a stage outweighed its
+// MFMAs (5-10 % slower).
 //
 // Per stage q: wait for this wavefront's LDS reads and for its loads of
 // stage q+1, one s_barrier (everyone's part of stage q+1 has landed and
@@ -175,6 +180,10 @@ struct DmaCursor {
   int q;              // its stage index (it stays on the last stage: later issues repeat it)
   int g;              // its group
   int u;              // its half of the layout step (E3M2 / E4M3)
+  // the step to the next stage inside a segment (see run_group): code and
+  // scale base increments when u is 0 / 1, and whether u alternates
+  int64_t inc0, inc1, sinc0, sinc1;
+  int flip;
   uint32_t doff[kCodeLoads];  // this lane's global byte offset for each code load of group g
   uint32_t mo[kCodeLoads];    // LDS offset (in a slot) of each code load of group g
 };
@@ -255,6 +264,45 @@ __device__ __forceinline__ void cursor_next(const DmaConst& k, const Stages& S, 
   }
   cur.bc = uni(cur.bc);
   cur.bs = uni(cur.bs);
+}
+
+// Point the cursor at stage qr for a run of stages whose refills stay in
+// qr's group (hold = true: every refill of the run is qr itself, the last
+// stage).  Only here do the group's per-lane offsets change.
+__device__ __forceinline__ void cursor_segment(const DmaConst& k, const Stages& S, DmaCursor& cur, int qr, bool hold,
+                                               int lane) {
+  const int g = stage_group(S, qr);
+  cursor_group(k, S, cur, g, qr, lane);  // the group's first stage, u = 0
+  if (g == 0) {
+    cur.bc = uni(cur.bc + (int64_t)qr * k.rstride0);
+    cur.bs = uni(cur.bs + (int64_t)qr * k.sstride);
+    cur.inc0 = cur.inc1 = k.rstride0;
+    cur.sinc0 = cur.sinc1 = k.sstride;
+    cur.flip = 0;
+  } else {
+    const int s = qr - (g == 1 ? S.q1 : S.q2);
+    const int64_t rs = g == 1 ? k.rstride1 : k.rstride2;
+    const int64_t gb = g == 1 ? stage_grp_bytes(1) : stage_grp_bytes(2);
+    cur.bc = uni(cur.bc + (int64_t)(s >> 1) * rs + (s & 1) * gb);
+    cur.bs = uni(cur.bs + (int64_t)(s >> 1) * k.sstride);
+    cur.u = s & 1;
+    cur.inc0 = gb;
+    cur.inc1 = rs - gb;
+    cur.sinc0 = 0;
+    cur.sinc1 = k.sstride;
+    cur.flip = 1;
+  }
+  if (hold) {
+    cur.inc0 = cur.inc1 = cur.sinc0 = cur.sinc1 = 0;
+    cur.flip = 0;
+  }
+}
+
+// One stage on inside a segment: no branch, the offsets untouched.
+__device__ __forceinline__ void cursor_step(DmaCursor& cur) {
+  cur.bc = uni(cur.bc + (cur.u ? cur.inc1 : cur.inc0));
+  cur.bs = uni(cur.bs + (cur.u ? cur.sinc1 : cur.sinc0));
+  cur.u ^= cur.flip;
 }
 
 // Load P of the stage the cursor points at, into the slot at LDS byte
@@ -446,11 +494,11 @@ __device__ __forceinline__ void stage(const Ctx<BN, BM>& c, Acc<BN, BM>& acc, Dm
   StageWork w;
   w.st_refill = __builtin_amdgcn_readfirstlane(st);
   w.ad = ops_addr<pattern(G), BN, BM>(st_next, opaque_s(c.wn0), opaque_s(c.wm0), c.lane);
-  // the cursor moves on before the MFMAs (its branches would otherwise end
-  // the MFMAs' basic block and let them sink away from the work they are
-  // interleaved with); this stage's refill uses the position it had
+  // the cursor moves on before the MFMAs (straight-line: a branch there
+  // would end the MFMAs' basic block and let them sink away from the work
+  // they are interleaved with); this stage's refill uses the position it had
   const DmaCursor issue = dc;
-  cursor_next(c.k, S, dc, c.lane);
+  cursor_step(dc);
   mfma_block<G, pattern(G), FS, 0>(acc, cur, sc, nxt, c.k, issue, w);
   st = st_next;
 }
@@ -465,14 +513,36 @@ __device__ __forceinline__ void run_group(const Ctx<BN, BM>& c, Acc<BN, BM>& acc
   const int qb = G == 0 ? 0 : (G == 1 ? c.S.q1 : c.S.q2);
   const int qe = G == 0 ? c.S.q1 : (G == 1 ? c.S.q2 : c.S.Q);
   if (qb == qe) return;
+  constexpr int NS = T::kSlots;
+  const Stages& S = c.S;
   Ops<BN, BM> A, B;
   read_items<pattern(G), 0, 2 * T::F>(A, ops_addr<pattern(G), BN, BM>(st, c.wn0, c.wm0, c.lane));
+  // segments: runs of stages whose refills (stage q + NS, the last one
+  // again past the end) stay in one group, so that inside a run the cursor
+  // only steps; it is re-pointed between runs
   int q = qb;
-  for (; q + 1 < qe; q += 2) {
-    stage<G, FS>(c, acc, dc, st, q, A, B);
-    stage<G, FS>(c, acc, dc, st, q + 1, B, A);
+  while (q < qe) {
+    const int qr = q + NS < S.Q ? q + NS : S.Q - 1;
+    const bool hold = q + NS >= S.Q - 1;
+    int e = qe;
+    if (!hold) {
+      const int gr = stage_group(S, qr);
+      if (gr == 0 && S.q1 - NS < e) e = S.q1 - NS;
+      if (gr <= 1 && S.q2 - NS < e) e = S.q2 - NS;
+      if (S.Q - 1 - NS < e) e = S.Q - 1 - NS;
+    }
+    e = e > q ? e : q + 1;
+    cursor_segment(c.k, S, dc, qr, hold, c.lane);
+    for (; q + 1 < e; q += 2) {
+      stage<G, FS>(c, acc, dc, st, q, A, B);
+      stage<G, FS>(c, acc, dc, st, q + 1, B, A);
+    }
+    if (q < e) {
+      stage<G, FS>(c, acc, dc, st, q, A, B);
+      A = B;  // the next run starts from A
+      ++q;
+    }
   }
-  if (q < qe) stage<G, FS>(c, acc, dc, st, q, A, B);
 }
 
 }  // namespace tiled
