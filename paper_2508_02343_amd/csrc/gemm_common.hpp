@@ -125,14 +125,23 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
+// Two fp32 values rounded to nearest even as a packed bf16 pair (a in the low
+// half): one gfx950 conversion instruction (v_cvt_pk_bf16_f32) instead of
+// the integer sequence above per value.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2_rne(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
 // Store lane's 4 consecutive output columns n..n+3 of row m.
 __device__ __forceinline__ void store_out4(const GemmArgs& a, int64_t m, int64_t n, const v4f& c, int64_t M,
                                            int64_t N) {
   if (m >= M) return;
   uint16_t* dst = a.y + m * a.ldy + n;
   if (n + 3 < N) {
-    const uint32_t lo = f32_to_bf16_rne(c[0]) | (f32_to_bf16_rne(c[1]) << 16);
-    const uint32_t hi = f32_to_bf16_rne(c[2]) | (f32_to_bf16_rne(c[3]) << 16);
+    const uint32_t lo = pack_bf16x2_rne(c[0], c[1]);
+    const uint32_t hi = pack_bf16x2_rne(c[2], c[3]);
     *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
   } else {
 #pragma unroll

@@ -655,8 +655,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int
     for (int j = 0; j < T::TM; ++j) {
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
-        const uint32_t lo = f32_to_bf16_rne(acc[i][j][4 * h]) | (f32_to_bf16_rne(acc[i][j][4 * h + 1]) << 16);
-        const uint32_t hi = f32_to_bf16_rne(acc[i][j][4 * h + 2]) | (f32_to_bf16_rne(acc[i][j][4 * h + 3]) << 16);
+        const uint32_t lo = pack_bf16x2_rne(acc[i][j][4 * h], acc[i][j][4 * h + 1]);
+        const uint32_t hi = pack_bf16x2_rne(acc[i][j][4 * h + 2], acc[i][j][4 * h + 3]);
         const uint32_t at = c.lds0 + (c.wm0 + 32 * j + r) * kRowStride + (c.wn0 + 32 * i + 8 * h + 4 * g) * 2;
         *reinterpret_cast<__attribute__((address_space(3))) u32x2*>((uintptr_t)at) = u32x2{lo, hi};
       }
