@@ -674,7 +674,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tiled_kernel(GemmArgs a, int
     const u32x4 v = lds_read<u32x4>(c.lds0 + rr * kRowStride + col * 2);
     uint16_t* dst = a.y + m * a.ldy + n;
     if (n + 8 <= N) {
-      *reinterpret_cast<u32x4*>(dst) = v;
+      // streamed: the output is not read again here, and keeping it out of
+      // the L2 leaves the operand panels of the tiles still running there
+      __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
     } else {
       for (int e = 0; e < (int)(N - n); ++e) {
         const uint32_t wd = e < 2 ? v.x : (e < 4 ? v.y : (e < 6 ? v.z : v.w));
