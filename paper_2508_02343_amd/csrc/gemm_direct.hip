@@ -4,10 +4,16 @@
 // columns so that the grid spans all CUs, and the workgroup's four or eight
 // wavefronts split the K loop between them and add their fp32 partial sums
 // in LDS before the single bf16 rounding (Sec. 3.2 "GEMM kernel": fp32
-// partials, bf16 out).  Each wavefront issues the loads of several of its
-// steps of a group before the first of their MFMAs, so it has that many
-// steps of weight in flight instead of a chain of one load, then one MFMA,
-// per step.
+// partials, bf16 out).
+//
+// Each wavefront works on the steps of one group only (the wavefronts are
+// shared out between the groups in proportion to their steps), so the loads
+// of all three groups are in flight at once instead of one group after the
+// other; inside its group a wavefront issues the loads of several steps
+// before the first of their MFMAs.  Per batch of steps, the E8M0 scales come
+// as one 4-byte word per lane and tile (the four block scales of one row at
+// one step) and reach the lanes that feed them to the MFMA through a
+// cross-lane read, instead of one single-byte load per lane and step.
 #include "gemm_common.hpp"
 
 namespace mm {
@@ -17,20 +23,46 @@ namespace mm {
 template <int TN, int TM>
 __host__ __device__ constexpr int direct_batch() { return TN * TM >= 8 ? 2 : 4; }
 
-// Group G's layout steps: wavefront w of W takes steps w, w + W, ..., U at
-// a time, issuing all U steps' loads before the first of their MFMAs.
-template <int TN, int TM, int W, int G, int FS>
+// The four E8M0 block scales of row n at global step t: one 4-byte word
+// (scale byte of block j at (t * rp + n) * 4 + j).
+__device__ __forceinline__ uint32_t load_scale_word(const uint8_t* sc, int64_t rp, int64_t t, int64_t n) {
+  return *(const __attribute__((address_space(1))) uint32_t*)(sc + (t * rp + n) * kStepBlocks);
+}
+
+// Group G's layout steps on the W wavefronts given to the group: wavefront
+// w takes steps w, w + W, ..., U at a time, all U steps' loads issued before
+// the first of their MFMAs.  Scale words: lane 16 u + r loads row r's word of
+// step u of the batch; the lane (block b, row r) that the MFMA of step u
+// takes the scale from reads that word from lane 16 u + r and shifts byte b
+// down.  Activation rows past the real ones are not loaded (zero codes, unit
+// scale): they only reach output rows that are never stored.
+template <int TN, int TM, int G, int FS>
 __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][TM], int64_t n0, int64_t m0,
-                                             int wave, int lane) {
+                                             int wave, int W, int lane) {
   constexpr int U = direct_batch<TN, TM>();
+  static_assert(U <= 4, "one scale word per lane holds the scales of four steps");
   const int S = a.steps[G];
-  if (S == 0) return;
   const int g = lane >> 4, r = lane & 15;
   // global step index of this group's first step inside the scale buffer
   const int t0 = (G >= 1 ? a.steps[0] : 0) + (G >= 2 ? a.steps[1] : 0);
   for (int s0 = wave; s0 < S; s0 += W * U) {
     v8i wf[U][TN], xf[U][TM];
-    int ws[U][TN], xs[U][TM];
+    uint32_t wsw[TN], xsw[TM];
+    {
+      const int su = s0 + W * g;  // step of this lane's scale words
+      const bool sval = g < U && su < S;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        int64_t n = n0 + 16 * i + r;
+        n = n < a.w.rp ? n : a.w.rp - 1;  // padded rows exist up to rp
+        wsw[i] = sval ? load_scale_word(a.w.sc, a.w.rp, t0 + su, n) : 0x7f7f7f7fu;
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int64_t m = m0 + 16 * j + r;
+        xsw[j] = sval && m < a.x.rows ? load_scale_word(a.x.sc, a.x.rp, t0 + su, m) : 0x7f7f7f7fu;
+      }
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = s0 + W * u;
@@ -38,51 +70,47 @@ __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][T
 #pragma unroll
         for (int i = 0; i < TN; ++i) {
           int64_t n = n0 + 16 * i + r;
-          n = n < a.w.rp ? n : a.w.rp - 1;  // padded rows exist up to rp
+          n = n < a.w.rp ? n : a.w.rp - 1;
           wf[u][i] = load_frag16_global<G>(a.w.q[G], a.w.rp, n, s, g);
-          ws[u][i] = load_scale(a.w.sc, a.w.rp, t0 + s, n, g);
         }
 #pragma unroll
         for (int j = 0; j < TM; ++j) {
-          int64_t m = m0 + 16 * j + r;
-          m = m < a.x.rp ? m : a.x.rp - 1;
-          xf[u][j] = load_frag16_global<G>(a.x.q[G], a.x.rp, m, s, g);
-          xs[u][j] = load_scale(a.x.sc, a.x.rp, t0 + s, m, g);
+          const int64_t m = m0 + 16 * j + r;
+          xf[u][j] = m < a.x.rows ? load_frag16_global<G>(a.x.q[G], a.x.rp, m, s, g) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
         }
       }
     }
     // all of the batch's loads are issued before its first MFMA
     __builtin_amdgcn_sched_barrier(0);
+    int ws[U][TN], xs[U][TM];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      // a step past the group's last (not loaded) adds exactly zero: zero
-      // codes (+0 in every element format) under the unit scale
-      const bool valid = s0 + W * u < S;
 #pragma unroll
-      for (int i = 0; i < TN; ++i) {
+      for (int i = 0; i < TN; ++i) ws[u][i] = __builtin_amdgcn_ds_bpermute((16 * u + r) * 4, (int)wsw[i]);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) wf[u][i][e] = valid ? wf[u][i][e] : 0;
-        ws[u][i] = valid ? ws[u][i] : 127;
-      }
+      for (int j = 0; j < TM; ++j) xs[u][j] = __builtin_amdgcn_ds_bpermute((16 * u + r) * 4, (int)xsw[j]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int j = 0; j < TM; ++j) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) xf[u][j][e] = valid ? xf[u][j][e] : 0;
-        xs[u][j] = valid ? xs[u][j] : 127;
-      }
+    for (int u = 0; u < U; ++u) {
+      if (s0 + W * u >= S) break;  // uniform: steps past the group's last were not loaded
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
-        for (int j = 0; j < TM; ++j) MM_MFMA_GROUP(G, FS, acc[i][j], wf[u][i], xf[u][j], ws[u][i], xs[u][j]);
+        for (int j = 0; j < TM; ++j)
+          MM_MFMA_GROUP(G, FS, acc[i][j], wf[u][i], xf[u][j], (int)((uint32_t)ws[u][i] >> (8 * g)),
+                        (int)((uint32_t)xs[u][j] >> (8 * g)));
     }
   }
 }
 
+// Wavefronts [0, w0) work on group 0, [w0, w0 + w1) on group 1, the next w2
+// on group 2; the partial sums are added in wavefront order.
 template <int TN, int TM, int W, int FS>
-__global__ __launch_bounds__(64 * W) void gemm_direct_kernel(GemmArgs a) {
-  __shared__ float red[W - 1][TN * TM * 4][64];
+__global__ __launch_bounds__(64 * W) void gemm_direct_kernel(GemmArgs a, int w0, int w1, int w2) {
+  __shared__ v4f red[W - 1][TN * TM][64];
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t n0 = (int64_t)blockIdx.x * (16 * TN);
   const int64_t m0 = (int64_t)blockIdx.y * (16 * TM);
 
@@ -92,17 +120,15 @@ __global__ __launch_bounds__(64 * W) void gemm_direct_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  direct_group<TN, TM, W, 0, FS>(a, acc, n0, m0, wave, lane);
-  direct_group<TN, TM, W, 1, FS>(a, acc, n0, m0, wave, lane);
-  direct_group<TN, TM, W, 2, FS>(a, acc, n0, m0, wave, lane);
+  if (wave < w0) direct_group<TN, TM, 0, FS>(a, acc, n0, m0, wave, w0, lane);
+  else if (wave < w0 + w1) direct_group<TN, TM, 1, FS>(a, acc, n0, m0, wave - w0, w1, lane);
+  else if (wave < w0 + w1 + w2) direct_group<TN, TM, 2, FS>(a, acc, n0, m0, wave - w0 - w1, w2, lane);
 
   if (wave > 0) {
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
-      for (int j = 0; j < TM; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) red[wave - 1][(i * TM + j) * 4 + q][lane] = acc[i][j][q];
+      for (int j = 0; j < TM; ++j) red[wave - 1][i * TM + j][lane] = acc[i][j];
   }
   __syncthreads();
   if (wave != 0) return;
@@ -113,17 +139,37 @@ __global__ __launch_bounds__(64 * W) void gemm_direct_kernel(GemmArgs a) {
     for (int j = 0; j < TM; ++j) {
       v4f c = acc[i][j];
 #pragma unroll
-      for (int w = 0; w < W - 1; ++w)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) c[q] += red[w][(i * TM + j) * 4 + q][lane];
+      for (int w = 0; w < W - 1; ++w) c += red[w][i * TM + j][lane];
       store_out4(a, m0 + 16 * j + r, n0 + 16 * i + 4 * g, c, a.x.rows, a.w.rows);
     }
+}
+
+// Wavefronts per group: one for each group that has steps, then one at a
+// time to the group whose wavefronts take the most steps each (ties: the
+// wider format), so the longest chain of steps is as short as it can be.
+static void direct_waves(const GemmArgs& a, int W, int* w) {
+  const int* S = a.steps;
+  for (int G = 0; G < 3; ++G) w[G] = S[G] > 0 ? 1 : 0;
+  for (int k = w[0] + w[1] + w[2]; k < W && k > 0; ++k) {
+    int best = -1, most = -1;
+    for (int G = 2; G >= 0; --G) {
+      if (w[G] == 0) continue;
+      const int c = (S[G] + w[G] - 1) / w[G];
+      if (c > most) {
+        most = c;
+        best = G;
+      }
+    }
+    ++w[best];
+  }
 }
 
 template <int TN, int TM, int W, int FS>
 static hipError_t launch_direct_fs(const GemmArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((a.w.rows + 16 * TN - 1) / (16 * TN)), (unsigned)((a.x.rows + 16 * TM - 1) / (16 * TM)));
-  hipLaunchKernelGGL((gemm_direct_kernel<TN, TM, W, FS>), grid, dim3(64 * W), 0, stream, a);
+  int w[3];
+  direct_waves(a, W, w);
+  hipLaunchKernelGGL((gemm_direct_kernel<TN, TM, W, FS>), grid, dim3(64 * W), 0, stream, a, w[0], w[1], w[2]);
   return hipGetLastError();
 }
 
