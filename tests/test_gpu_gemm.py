@@ -68,6 +68,22 @@ def test_ragged(M, N, split):
     _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
 
 
+@pytest.mark.parametrize("M,N,split", [(1, 6001, (96, 160, 96)), (20, 6000, (256, 128, 128)),
+                                       (50, 6000, (0, 0, 512)), (1, 12000, (256, 128, 128)),
+                                       (20, 12000, (96, 160, 96)), (50, 12000, (256, 128, 128)),
+                                       (8, 20008, (256, 128, 128)), (64, 20000, (0, 0, 512))])
+def test_decode_strips(M, N, split):
+    """Decode kernel (M <= 64) at the strip widths its launch picks: for one
+    activation tile 16-row strips (N = 6001) or whole 32-row groups
+    (N = 12000, 20008: a part-filled last group); for two or four activation
+    tiles rows per workgroup that are not a multiple of 16 (24, 48 and 40 on
+    256 CUs: part-filled last tiles, two or four tiles per workgroup), the
+    last at a width that needs two workgroups per CU."""
+    note(f"decode strips M={M} N={N} split={split}")
+    xb, wb, perm = _rand_case(M, N, split, seed=M * 11 + N + split[0])
+    _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
+
+
 @pytest.mark.parametrize("split", [(96, 160, 96), (352, 0, 0), (0, 352, 0), (0, 0, 352), (128, 0, 224)])
 @pytest.mark.parametrize("M,N", [(3000, 5400), (1000, 1000)])
 def test_ragged_large(M, N, split):
