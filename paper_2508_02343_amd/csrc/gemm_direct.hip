@@ -8,7 +8,7 @@
 // and the number of wavefronts only, not on which strip holds it.
 //
 // Each wavefront works on the steps of one group only (the wavefronts are
-// shared out between the groups in proportion to their steps), so the loads
+// shared out between the groups by their numbers of steps), so the loads
 // of all three groups are in flight at once instead of one group after the
 // other; inside its group a wavefront issues the loads of several steps
 // before the first of their MFMAs.  Per batch of steps, the E8M0 scales come
@@ -36,8 +36,9 @@ __device__ __forceinline__ uint32_t load_scale_word(const uint8_t* sc, int64_t r
 // the first of their MFMAs.  Scale words: lane 16 u + r loads row r's word of
 // step u of the batch; the lane (block b, row r) that the MFMA of step u
 // takes the scale from reads that word from lane 16 u + r and shifts byte b
-// down.  Activation rows past the real ones are not loaded (zero codes, unit
-// scale): they only reach output rows that are never stored.
+// down.  Weight rows past the strip (R) or past N, and activation rows past
+// the real ones, are not loaded (zero codes, unit scale): they only reach
+// outputs that are never stored.
 template <int TN, int TM, int G, int FS>
 __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][TM], int64_t n0, int R, int64_t m0,
                                              int wave, int W, int lane) {
