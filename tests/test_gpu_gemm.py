@@ -84,6 +84,17 @@ def test_decode_strips(M, N, split):
     _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
 
 
+@pytest.mark.parametrize("M,N", [(4, 700), (24, 300)])
+def test_decode_long_k(M, N):
+    """Decode kernel on the MLP-down width (K = 14336, split 10752 / 2688 / 896:
+    84, 21 and 7 steps): the eight wavefronts go 5 / 2 / 1 to the groups, so
+    every group takes several batches of steps per wavefront."""
+    split = (10752, 2688, 896)
+    note(f"decode long K M={M} N={N}")
+    xb, wb, perm = _rand_case(M, N, split, seed=M + N)
+    _check_full(xb, wb, perm, split, f"M{M} N{N} {split}")
+
+
 @pytest.mark.parametrize("split", [(96, 160, 96), (352, 0, 0), (0, 352, 0), (0, 0, 352), (128, 0, 224)])
 @pytest.mark.parametrize("M,N", [(3000, 5400), (1000, 1000)])
 def test_ragged_large(M, N, split):
