@@ -473,9 +473,13 @@ __device__ __forceinline__ const uint8_t* uni_ptr(const uint8_t* p) {
 
 // Direct global -> LDS load: lane i's 16 bytes at sbase + voff land at M0 +
 // 16 i.  Inline asm, so the compiler neither tracks nor waits for it; the
-// producers' explicit vmcnt waits do.  The s_nop covers the M0 write.
+// producers' explicit vmcnt waits do.  The s_nop covers the M0 write.  The
+// rows are read once, so the load is marked non-temporal (nt): their lines
+// go first when the L2 evicts, and the partly written lines of the packed
+// codes (runs of a few rows that other workgroups complete) stay there to be
+// merged (8192 x 5120: 31.6 -> 28.6 us).
 __device__ __forceinline__ void dma16(uint32_t voff, const uint8_t* sbase, uint32_t lds) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase), "{m0}"(lds) : "memory");
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt" : : "v"(voff), "s"(sbase), "{m0}"(lds) : "memory");
 }
 
 // Square sums of the rows of the pass in the slot at `slot` (row r at r *
