@@ -31,8 +31,13 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// kStream: a non-temporal load (data read once: its L2 lines go first).
+template <bool kStream = false>
 __device__ __forceinline__ uint4 gload16(const void* p) {
-  const u32x4 v = *(const __attribute__((address_space(1))) u32x4*)(p);
+  const __attribute__((address_space(1))) u32x4* q = (const __attribute__((address_space(1))) u32x4*)(p);
+  u32x4 v;
+  if constexpr (kStream) v = __builtin_nontemporal_load(q);
+  else v = *q;
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 __device__ __forceinline__ uint2 gload8(const void* p) {
@@ -50,12 +55,15 @@ __host__ __device__ constexpr int group_fmt(int group, int fs) {
 
 // One lane's 16 x 128 operand fragment (16 x 16 x 128 form, lane 16 g + r)
 // straight from the packed layout: row n, step `step` of group G.  The padded
-// layout makes every step whole, so there is no bounds logic here.
-template <int G>
+// layout makes every step whole, so there is no bounds logic here.  kStream
+// makes the E2M1 and E4M3 loads non-temporal; the E3M2 ones stay plain (a
+// lane's 24 bytes come in two loads whose cache lines other lanes share, and
+// streamed lines can be gone before the second load).
+template <int G, bool kStream = false>
 __device__ __forceinline__ v8i load_frag16_global(const uint8_t* base, int64_t rp, int64_t n, int64_t step, int g) {
   v8i v;
   if constexpr (G == 0) {
-    const uint4 d = gload16(base + code_offset<0>(step, rp, n, g));
+    const uint4 d = gload16<kStream>(base + code_offset<0>(step, rp, n, g));
     v[0] = (int)d.x;
     v[1] = (int)d.y;
     v[2] = (int)d.z;
@@ -75,8 +83,8 @@ __device__ __forceinline__ v8i load_frag16_global(const uint8_t* base, int64_t r
     // channels 16g .. 16g+15: block g/2, half g%2, i.e. record slot g; and
     // channels 64+16g ..: block 2 + g/2, half g%2, record slot 4 + g
     const uint8_t* s = base + code_offset<2>(step, rp, n, 0);
-    const uint4 lo = gload16(s + g * 512);
-    const uint4 hi = gload16(s + (4 + g) * 512);
+    const uint4 lo = gload16<kStream>(s + g * 512);
+    const uint4 hi = gload16<kStream>(s + (4 + g) * 512);
     v[0] = (int)lo.x;
     v[1] = (int)lo.y;
     v[2] = (int)lo.z;

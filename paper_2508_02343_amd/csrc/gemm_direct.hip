@@ -38,7 +38,8 @@ __device__ __forceinline__ uint32_t load_scale_word(const uint8_t* sc, int64_t r
 // takes the scale from reads that word from lane 16 u + r and shifts byte b
 // down.  Weight rows past the strip (R) or past N, and activation rows past
 // the real ones, are not loaded (zero codes, unit scale): they only reach
-// outputs that are never stored.
+// outputs that are never stored.  The weight is read once: its E2M1 and E4M3
+// loads are non-temporal (N = 14336 E4M3: 12.7 -> 11.9 us).
 template <int TN, int TM, int G, int FS>
 __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][TM], int64_t n0, int R, int64_t m0,
                                              int wave, int W, int lane) {
@@ -72,7 +73,7 @@ __device__ __forceinline__ void direct_group(const GemmArgs& a, v4f (&acc)[TN][T
 #pragma unroll
         for (int i = 0; i < TN; ++i) {
           const int64_t n = n0 + 16 * i + r;
-          wf[u][i] = 16 * i + r < R && n < a.w.rows ? load_frag16_global<G>(a.w.q[G], a.w.rp, n, s, g)
+          wf[u][i] = 16 * i + r < R && n < a.w.rows ? load_frag16_global<G, true>(a.w.q[G], a.w.rp, n, s, g)
                                                      : v8i{0, 0, 0, 0, 0, 0, 0, 0};
         }
 #pragma unroll
