@@ -57,6 +57,14 @@ __device__ __forceinline__ void add_word(double* s, uint32_t& mx, uint32_t w) {
   mx = max(mx, max(lo, hi));
 }
 
+// 16 bytes of X, non-temporal: every byte is read once, so its L2 lines go
+// first (32768 x 14336: 191 -> 172 us for the whole call).
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_x16(const uint16_t* p) {
+  const u32x4_nt v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ void add_row(double* s, uint32_t& mx, uint4 v) {
   add_word(s + 0, mx, v.x);
   add_word(s + 2, mx, v.y);
@@ -124,11 +132,11 @@ __global__ __launch_bounds__(64 * kSumWaves) void colsum_kernel(CalibArgs a) {
     for (; r + (U - 1) * kSumWaves < r1; r += U * kSumWaves) {
       uint4 v[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) v[u] = *reinterpret_cast<const uint4*>(p + (r + u * kSumWaves) * a.ldx);
+      for (int u = 0; u < U; ++u) v[u] = load_x16(p + (r + u * kSumWaves) * a.ldx);
 #pragma unroll
       for (int u = 0; u < U; ++u) add_row(s, mx, v[u]);
     }
-    for (; r < r1; r += kSumWaves) add_row(s, mx, *reinterpret_cast<const uint4*>(p + r * a.ldx));
+    for (; r < r1; r += kSumWaves) add_row(s, mx, load_x16(p + r * a.ldx));
   }
   mx = wave_max(mx);
   if (lane == 0) wmax[wave] = mx;
