@@ -782,9 +782,8 @@ static hipError_t launch_ring(const QuantArgs& a, hipStream_t stream, bool* used
   // more passes to overlap (Llama 2048 x 4096: 9.6 -> 8.8 us; with the norm
   // the producers' row sums then lose half their wavefronts, so not there)
   while (a.norm == 0 && rpp >= 4 && (a.rp + rpp - 1) / rpp < 4 * (int64_t)cus) rpp /= 2;
-  // one row per pass (K > 8192): the pipelined kernel, with two workgroups
-  // and twice the quantising wavefronts per CU, measured faster (K = 14336:
-  // 35 us against 42 us for 4096 rows)
+  // one row per pass (K > 8192): the pipelined kernel measured faster
+  // there (K = 14336: 35 us against 42 us for 4096 rows)
   if (rpp < 2) return hipSuccess;
   // per-lane load offsets are 32-bit, relative to the pass's first row
   if ((int64_t)rpp * a.ldx * 2 + (int64_t)K * 2 >= ((int64_t)1 << 32)) return hipSuccess;
