@@ -777,11 +777,12 @@ static hipError_t launch_ring(const QuantArgs& a, hipStream_t stream, bool* used
   int cus = 0;
   hipError_t e = device_cus(&cus);
   if (e != hipSuccess) return e;
-  // few rows (under four passes per workgroup), plain quantiser: halve the
+  // few rows (under eight passes per workgroup), plain quantiser: halve the
   // pass while it keeps two or more rows, so that each workgroup's ring has
-  // more passes to overlap (Llama 2048 x 4096: 9.6 -> 8.8 us; with the norm
-  // the producers' row sums then lose half their wavefronts, so not there)
-  while (a.norm == 0 && rpp >= 4 && (a.rp + rpp - 1) / rpp < 4 * (int64_t)cus) rpp /= 2;
+  // more passes to overlap (2048 x 4096: 9.6 -> 8.8 us; 4096 x 4096, with
+  // the streamed loads: 15.5 -> 14.1 us; with the norm the producers' row
+  // sums then lose half their wavefronts, so not there)
+  while (a.norm == 0 && rpp >= 4 && (a.rp + rpp - 1) / rpp < 8 * (int64_t)cus) rpp /= 2;
   // one row per pass (K > 8192): the pipelined kernel measured faster
   // there (K = 14336: 35 us against 42 us for 4096 rows)
   if (rpp < 2) return hipSuccess;
